@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""Benchmark of the AVTP pruning layer on one MI355X.
+
+One step = one pruning layer over one batch: row statistics + column-sum
+score passes, per-image budgets, segmented top-k, and the compaction of
+hidden states, position ids and the layer's K and V.  Inputs are seeded
+synthetic tensors already resident in HBM.
+
+    python bench.py [--steps K] [--warmup W] [--config 5] [--no-cpu-baseline]
+
+Prints one JSON line.  ``value`` is visual tokens processed per second for
+the whole layer; ``roofline`` describes the dominant kernel (timed live with
+HIP events on the stream the library launches on); ``cpu_baseline`` times the
+float64 CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+METRIC = ("µs per pruning layer + visual tokens scored/s; % MFMA peak (score), "
+          "% HBM peak")
+PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA, MI355X
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def algorithmic_counts(lay, Hq, d, row_bytes_total):
+    """Per-launch algorithmic work of each stage.
+
+    pass 1: one q.k product per (head, text row, key at or before the row)
+    pass 2: one per (head, text row, visual key before the row)
+    compaction: each kept row read once and written once, plus its index.
+    """
+    vis = lay.visual_mask()
+    p1 = p2 = 0
+    for b in range(lay.B):
+        s0 = int(lay.cu_seqlens[b])
+        cum = np.cumsum(vis[s0:int(lay.cu_seqlens[b + 1])])
+        for t in range(int(lay.cu_text[b]), int(lay.cu_text[b + 1])):
+            p = int(lay.text_pos[t]) - s0
+            p1 += p + 1
+            p2 += int(cum[p])
+    flops1 = 2.0 * d * Hq * p1
+    flops2 = 2.0 * d * Hq * p2
+    comp_bytes = 2.0 * lay.N_out * row_bytes_total + 4.0 * lay.N_out
+    sel_bytes = 4.0 * lay.N_tok + 4.0 * lay.N_out + 8.0 * lay.n_img
+    return flops1, flops2, comp_bytes, sel_bytes
+
+
+def cpu_baseline(wl):
+    """The float64 oracle on one sequence of the workload (score, budget,
+    select, compaction of that sequence's hidden states)."""
+    from oracle import avtp_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    lay = wl.layout
+    b = 0
+    t0 = time.perf_counter()
+    s, isum, _, _ = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale, wl.dtype,
+                                  seqs=[b])
+    i0, i1 = int(lay.cu_img[b]), int(lay.cu_img[b + 1])
+    # budget and selection of sequence b only
+    from paper_2608_26806_amd.workloads import Layout
+    s0, s1 = int(lay.cu_seqlens[b]), int(lay.cu_seqlens[b + 1])
+    ta, tb = int(lay.cu_text[b]), int(lay.cu_text[b + 1])
+    sub = Layout(np.array([0, s1 - s0], np.int32), (lay.img_start[i0:i1] - s0).astype(np.int32),
+                 lay.img_len[i0:i1].copy(), np.array([0, i1 - i0], np.int32),
+                 (lay.text_pos[ta:tb] - s0).astype(np.int32), np.array([0, tb - ta], np.int32),
+                 lay.keep_total[b:b + 1].copy())
+    bud = O.budget(sub, isum[i0:i1].astype(np.float32), wl.alpha, wl.lo_permille, wl.hi_permille,
+                   wl.floor_abs)
+    keep, _ = O.select(sub, s[s0:s1].astype(np.float32), bud)
+    O.compact(keep, wl.hidden_states[s0:s1])
+    dt = time.perf_counter() - t0
+    m = int(lay.img_len[i0:i1].sum())
+    return {"value": m / dt, "unit": "visual tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"sequence 0 of the workload ({m} visual tokens, {tb - ta} text rows), "
+                      f"all four stages, float64 numpy; {dt:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(the per-sequence path shards over sequences, see DESIGN.md)"}))
+        sys.exit(2)
+    import torch
+    from paper_2608_26806_amd import avtp as A
+    from paper_2608_26806_amd.workloads import CONFIGS, make_workload
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    wl = make_workload(args.config, payload=True)
+    lay = wl.layout
+    gen_s = time.perf_counter() - t_gen
+
+    def up(x):
+        if wl.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(dev)
+
+    dl = A.DeviceLayout(lay, device=dev)
+    q, k, v = up(wl.q_text), up(wl.k), up(wl.v)
+    hid = up(wl.hidden_states)
+    pos = torch.from_numpy(wl.pos).to(dev)
+    dt = A.dtype_code(q)
+    ws = A.alloc_workspace(A.score_workspace_bytes(dl, A.SCORE_ATTN, dt, wl.Hq, wl.Hkv, wl.d), dev)
+    lse = torch.empty((wl.Hq, lay.T_tot), dtype=torch.float32, device=dev)
+    scores = torch.empty(lay.N_tok, dtype=torch.float32, device=dev)
+    isum = torch.empty(max(1, lay.n_img), dtype=torch.float32, device=dev)
+    bud = torch.empty(max(1, lay.n_img), dtype=torch.int32, device=dev)
+    keep = torch.empty(lay.N_out, dtype=torch.int32, device=dev)
+    cu_out = torch.empty(lay.B + 1, dtype=torch.int32, device=dev)
+    status = torch.zeros(lay.B, dtype=torch.int32, device=dev)
+    outs = []
+    pairs = []
+    for src, tdim in [(hid, 0), (pos, 1), (k, 0), (v, 0)]:
+        shape = list(src.shape)
+        shape[tdim] = lay.N_out
+        dst = torch.empty(shape, dtype=src.dtype, device=dev)
+        outs.append(dst)
+        pairs.append((src, dst, tdim))
+    row_bytes_total = sum(p[0][0].numel() * p[0].element_size() if p[2] == 0 else
+                          p[0].shape[0] * p[0][0, 0].numel() * p[0].element_size() for p in pairs)
+
+    stream = torch.cuda.current_stream()
+    names = ["row_lse", "score", "budget", "select", "compact"]
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        A.row_lse(dl, q, k, wl.softmax_scale, out=lse, ws=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        A.score_attn(dl, q, k, wl.softmax_scale, row_lse=lse, scores=scores, img_sum=isum,
+                     status=status, ws=ws)
+        if ev is not None:
+            ev[2].record(stream)
+        A.budget(dl, isum, wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs, out=bud,
+                 status=status)
+        if ev is not None:
+            ev[3].record(stream)
+        A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status)
+        if ev is not None:
+            ev[4].record(stream)
+        A.compact(dl, keep, pairs)
+        if ev is not None:
+            ev[5].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([[events[i][j].elapsed_time(events[i][j + 1]) for j in range(5)]
+                    for i in range(args.steps)])          # ms
+    layer_ms = np.array([events[i][0].elapsed_time(events[i][5]) for i in range(args.steps)])
+    st = status.cpu().numpy()
+    if st.any():
+        print(f"warning: device status flags {st.tolist()}", file=sys.stderr)
+
+    M = int(lay.img_len.sum())
+    ms_layer = float(np.median(layer_ms))
+    ms = {n: float(np.mean(per[:, j])) for j, n in enumerate(names)}
+    f1, f2, comp_bytes, sel_bytes = algorithmic_counts(lay, wl.Hq, wl.d, row_bytes_total)
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
+    tf1 = f1 / (ms["row_lse"] * 1e-3) / 1e12
+    tf2 = f2 / (ms["score"] * 1e-3) / 1e12
+    dom = "row_lse" if ms["row_lse"] >= ms["score"] else "score"
+    ach = tf1 if dom == "row_lse" else tf2
+    comp_gbs = comp_bytes / (ms["compact"] * 1e-3) / 1e9
+    selcomp_gbs = (comp_bytes + sel_bytes) / ((ms["compact"] + ms["select"]) * 1e-3) / 1e9
+    value = M / (ms_layer * 1e-3)
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "visual tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_layer,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded; shapes of the paper's LVLMs, no datasets or weights)",
+        "config": {"workload": f"config {args.config}: {CONFIGS[args.config]['name']}",
+                   "batch": lay.B, "visual_tokens": M, "text_rows": lay.T_tot,
+                   "N_tok": lay.N_tok, "N_out": lay.N_out, "Hq": wl.Hq, "Hkv": wl.Hkv,
+                   "head_dim": wl.d, "hidden": wl.hidden, "score_mode": "attn",
+                   "parallelism": "none (1 GPU)"},
+        "us_per_layer": ms_layer * 1e3,
+        "us_per_call": {n: ms[n] * 1e3 for n in names},
+        "visual_tokens_scored_per_s": M / ((ms["row_lse"] + ms["score"]) * 1e-3),
+        "roofline": {
+            "kernel": "pass 1: row statistics (rowstats + lse combine)" if dom == "row_lse"
+                      else "pass 2: column sums (colsum + finalize)",
+            "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+            "frac": ach / peak, "traffic": None},
+        "score_passes": {
+            "pass1_alg_gflop": f1 / 1e9, "pass1_tflops": tf1, "pass1_frac": tf1 / peak,
+            "pass2_alg_gflop": f2 / 1e9, "pass2_tflops": tf2, "pass2_frac": tf2 / peak,
+            "both_passes_frac": (f1 + f2) / ((ms["row_lse"] + ms["score"]) * 1e-3) / 1e12 / peak},
+        "roofline_compact": {"bound": "hbm", "achieved": comp_gbs, "peak": PEAK_HBM_GBS,
+                             "unit": "GB/s", "frac": comp_gbs / PEAK_HBM_GBS,
+                             "alg_bytes": comp_bytes},
+        "select_plus_compact_hbm_frac": selcomp_gbs / PEAK_HBM_GBS,
+        "wall_s_timed_region": wall,
+        "input_generation_s": gen_s,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,210 @@
+/*
+ * avtp.h -- C ABI of libavtp.so, the MI355X (gfx950) pruning-layer operator of
+ * "Multi-Image Visual Token Pruning in Large Visual Language Models" (AVTP).
+ *
+ * A pruning layer turns the n visual tokens of each sequence into a shorter
+ * subsequence (Method, "Visual Token Pruning": E_pruned = p(E_v)).  The four
+ * calls below are the four steps of that map:
+ *
+ *   avtp_score   importance of every visual token and its per-image sum
+ *   avtp_budget  per-image keep counts from the image importances
+ *   avtp_select  per-image top-k -> ascending list of kept token indices
+ *   avtp_compact gather of hidden states, position ids and the layer's K/V
+ *
+ * Conventions shared by every call
+ *   - Every data pointer is caller-owned DEVICE memory unless its name starts
+ *     with h_ or the comment says "host".  The library allocates nothing.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = null stream).
+ *     Argument errors are detected on the host, before anything is enqueued,
+ *     and returned synchronously; nothing is launched in that case.
+ *   - Return value: AVTP_OK or a negative avtp_status.  HIP launch errors map
+ *     to AVTP_ERR_HIP.
+ *   - Data-dependent conditions found on the device are OR-ed into the
+ *     optional per-sequence status word (int32 [B], caller zero-fills it).
+ *   - Outputs must not alias inputs.  No global mutable state: calls on
+ *     different streams with different buffers may run concurrently.
+ */
+#ifndef AVTP_H
+#define AVTP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void *avtp_stream_t; /* a hipStream_t */
+
+typedef enum {
+  AVTP_OK = 0,
+  AVTP_ERR_INVALID_ARG = -1, /* null pointer, inconsistent layout, bad size */
+  AVTP_ERR_UNSUPPORTED = -2, /* head_dim, dtype, or a size beyond the limits below */
+  AVTP_ERR_INFEASIBLE = -3,  /* keep_total outside [sum of lower, sum of upper bounds] */
+  AVTP_ERR_WORKSPACE = -4,   /* workspace missing or smaller than *_workspace_size */
+  AVTP_ERR_HIP = -5          /* a HIP launch failed */
+} avtp_status;
+
+typedef enum { AVTP_BF16 = 0, AVTP_FP32 = 1 } avtp_dtype;
+
+typedef enum {
+  AVTP_SCORE_ATTN = 0,      /* attention paid by the text rows to each visual token */
+  AVTP_SCORE_VARIATION = 1  /* 1 - cos(h^l, h^prior), the hidden-state variation  */
+} avtp_score_mode;
+
+typedef enum {
+  AVTP_BUDGET_PROPORTIONAL = 0, /* keep ratio scaled by importance / mean importance */
+  AVTP_BUDGET_RAW = 1           /* keep ratio shifted by alpha (importance - mean)   */
+} avtp_budget_mode;
+
+/* per-sequence device status bits */
+#define AVTP_FLAG_NAN_SCORE 1       /* a visual score was NaN (ranked last)           */
+#define AVTP_FLAG_NO_TEXT_AFTER 2   /* an image has no text row after it (scores = 0) */
+#define AVTP_FLAG_INFEASIBLE 4      /* budget bounds cannot meet keep_total           */
+#define AVTP_FLAG_OUT_CAPACITY 8    /* kept list longer than keep_capacity (truncated) */
+
+/* Limits checked on the host (AVTP_ERR_UNSUPPORTED beyond them). */
+#define AVTP_MAX_IMAGES_PER_SEQ 256
+#define AVTP_MAX_IMAGES 8192
+#define AVTP_MAX_IMAGE_LEN (1 << 20)
+#define AVTP_MAX_TENSORS 8
+
+/*
+ * Packed ("THD") description of one batch of B sequences, N_tok tokens.
+ * Sequence b owns tokens [cu_seqlens[b], cu_seqlens[b+1]).  Every token is
+ * either a text token or belongs to exactly one image:
+ *   image i: tokens [img_start[i], img_start[i] + img_len[i]) (global
+ *            indices); the images of sequence b are cu_img[b] .. cu_img[b+1]-1,
+ *            in ascending position order;
+ *   text t:  token text_pos[t]; the text rows of sequence b are
+ *            cu_text[b] .. cu_text[b+1]-1, in ascending position order.
+ * keep_total[b] is the number of visual tokens sequence b keeps.
+ * Each int32 array is given twice: as device memory (read by the kernels)
+ * and as a host mirror with identical contents (read by the host-side
+ * validation and launch sizing; never dereferenced on the device).
+ */
+typedef struct {
+  int32_t B, n_img, N_tok, T_tot;
+  const int32_t *cu_seqlens, *img_start, *img_len, *cu_img, *text_pos, *cu_text, *keep_total;
+  const int32_t *h_cu_seqlens, *h_img_start, *h_img_len, *h_cu_img, *h_text_pos, *h_cu_text,
+      *h_keep_total;
+} avtp_layout;
+
+/*
+ * One tensor to compact.  For every plane p < planes and output row r:
+ *   dst + p*dst_plane_stride + r*dst_stride  <-  row_bytes bytes from
+ *   src + p*src_plane_stride + keep_idx[r]*src_stride
+ * (token-major [N_tok, ...] tensors use planes = 1; position ids [P, N_tok]
+ * use planes = P; head-major K/V [Hkv, N_tok, d] use planes = Hkv).
+ * All strides and offsets in bytes.
+ */
+typedef struct {
+  const void *src;
+  void *dst;
+  int64_t row_bytes, src_stride, dst_stride;
+  int32_t planes;
+  int64_t src_plane_stride, dst_plane_stride;
+} avtp_tensor;
+
+/* ------------------------------------------------------------------------
+ * avtp_score -- importance of every visual token.
+ *
+ * AVTP_SCORE_ATTN (the attention a layer pays to visual tokens, the quantity
+ * summed in Sec. 3.3.2, here kept per token).  With c = softmax_scale, query
+ * head h using key head g = h / (Hq/Hkv) (grouped-query attention), text row t
+ * at position p_t and the causal row normaliser
+ *   lse[h,t] = log sum_{j <= p_t, j in seq} exp(c q_{t,h}.k_{j,g}),
+ * the score of visual token j is
+ *   s_j = 1/Hq sum_h 1/|T_j| sum_{t in T_j} exp(c q_{t,h}.k_{j,g} - lse[h,t])
+ * where T_j are the text rows after j.  Computed in two tiled passes over
+ * the keys (row statistics, then column sums) with bf16 MFMA and fp32
+ * accumulation; the attention matrix is never stored.  If row_lse is given
+ * (e.g. the softmax LSE of the layer's own fused attention, natural log,
+ * [Hq, T_tot] fp32) the first pass is skipped.
+ *   q_text [T_tot, Hq, d]  queries of the text rows (dtype)
+ *   k      [N_tok, Hkv, d] the layer's keys (dtype)
+ *   d in {64, 128}, Hq % Hkv == 0.
+ *
+ * AVTP_SCORE_VARIATION (Sec. 3.3.1, importance = 1 - Sim(h^l, h^prior),
+ * Sim = cosine similarity with a 1e-8 norm guard):
+ *   h_cur, h_prior [N_tok, hidden] (dtype); q_text, k, row_lse unused.
+ *
+ * Outputs: scores [N_tok] fp32 (+inf at text positions), img_sum [n_img]
+ * fp32 = sum of the image's scores (Sec. 3.3.3 mean importance times |V_i|).
+ * An image with no text row after it scores 0 and flags
+ * AVTP_FLAG_NO_TEXT_AFTER.  Deterministic: bit-identical key rows in one
+ * image give bit-identical scores, and reruns are bit-identical.
+ * ws: device scratch of at least avtp_score_workspace_size() bytes (0 for an
+ * invalid layout or arguments); its contents need no initialisation.
+ * ---------------------------------------------------------------------- */
+size_t avtp_score_workspace_size(const avtp_layout *layout, int mode, int dtype, int Hq, int Hkv,
+                                 int d);
+int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dtype,
+               const void *q_text, const void *k, int Hq, int Hkv, int d, float softmax_scale,
+               const float *row_lse, const void *h_cur, const void *h_prior, int hidden,
+               float *scores, float *img_sum, int32_t *status, void *ws, size_t ws_bytes);
+
+/* The first pass of AVTP_SCORE_ATTN alone: row_lse_out [Hq, T_tot] fp32,
+ * natural-log LSE of each text row's causal attention logits (definition
+ * above).  Same arguments and workspace as avtp_score. */
+int avtp_row_lse(avtp_stream_t stream, const avtp_layout *layout, int dtype, const void *q_text,
+                 const void *k, int Hq, int Hkv, int d, float softmax_scale, float *row_lse_out,
+                 void *ws, size_t ws_bytes);
+
+/* ------------------------------------------------------------------------
+ * avtp_budget -- per-image keep counts (Sec. 3.3.3 ratio rule, clamp of the
+ * appendix on alpha).  For sequence b with images of n_i tokens and sums S_i,
+ * M = sum n_i, S = sum S_i, K = keep_total[b]:
+ *   PROPORTIONAL: quota share w_i = (1-alpha) n_i/M + alpha S_i/S
+ *   RAW:          w_i = n_i/M + alpha (S_i - n_i S/M) / K
+ * (each the ratio r_i = r_base + alpha (Ibar_i - Ibar_avg) of the paper with
+ * r_base = K/M; PROPORTIONAL measures importance in units of its mean).
+ * w_i < 0 -> 0; W_i = max(1, rint(w_i * 2^28)), float64, no FMA contraction;
+ * if S is not positive and finite, w_i = n_i/M.  Bounds
+ *   lo_i = min(n_i, max(ceil(lo_permille n_i / 1000), floor_abs)),
+ *   hi_i = max(lo_i, floor(hi_permille n_i / 1000))
+ * (paper: 5 % and 95 %, i.e. 50 and 950).  Exact integer water-filling finds
+ * q_i = clamp(lam W_i, lo_i, hi_i) with sum q_i = K; largest-remainder
+ * rounding (ties to the lowest image index) gives budget[i], sum = K.
+ * alpha in [0, 32].  AVTP_ERR_INFEASIBLE (host check) if K is outside
+ * [sum lo_i, sum hi_i].  budget: [n_img] int32 output.
+ * ---------------------------------------------------------------------- */
+int avtp_budget(avtp_stream_t stream, const avtp_layout *layout, const float *img_sum, int mode,
+                float alpha, int lo_permille, int hi_permille, int floor_abs, int32_t *budget,
+                int32_t *status);
+
+/* ------------------------------------------------------------------------
+ * avtp_select -- keep, inside every image, the budget[i] highest-scoring
+ * tokens (score descending; an exact tie keeps the lowest token index; -0.0
+ * equals +0.0; NaN ranks last), plus every text token.  Writes the kept
+ * global token indices of each sequence in ascending order to
+ * keep_idx[cu_out[b] .. cu_out[b+1]), and cu_out [B+1].
+ * keep_capacity: entries available in keep_idx; must be at least
+ * T_tot + sum(keep_total) (checked on the host); writes past it are dropped
+ * and flag AVTP_FLAG_OUT_CAPACITY (budgets not summing to keep_total).
+ * ---------------------------------------------------------------------- */
+int avtp_select(avtp_stream_t stream, const avtp_layout *layout, const float *scores,
+                const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out,
+                int32_t *status);
+
+/* ------------------------------------------------------------------------
+ * avtp_compact -- stable gather out[r] = in[keep_idx[r]] for up to
+ * AVTP_MAX_TENSORS tensors in one launch (hidden states, position ids with
+ * their original values, K and V of the layer).  n_out = number of entries
+ * of keep_idx to apply (normally T_tot + sum(keep_total)); every keep_idx
+ * entry must lie in [0, N_tok).  tensors: HOST array of n_tensors
+ * descriptors.  Copies are bit-exact.
+ * ---------------------------------------------------------------------- */
+int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,
+                 int64_t n_out, const avtp_tensor *tensors, int n_tensors);
+
+/* Human-readable name of an avtp_status value (static string). */
+const char *avtp_status_string(int status);
+
+/* ABI version: (major << 16) | minor. */
+int avtp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AVTP_H */

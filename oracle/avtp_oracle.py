@@ -210,6 +210,7 @@ def variation_scores(layout, h_cur, h_prior, dtype: str):
 # O2: per-image budgets (Sec. 3.3.3 + Appendix clamp)
 # ---------------------------------------------------------------------------
 WEIGHT_BITS = 28          # the quantisation grid of the per-image weights
+WEIGHT_CAP = 64.0         # largest per-image weight
 BUDGET_PROPORTIONAL = 0   # r_i in units where the mean importance equals r_base
 BUDGET_RAW = 1            # r_i = r_base + alpha (I_i - I_avg) in raw score units
 
@@ -231,7 +232,8 @@ def budget_weights(n_list, S_list, K: int, alpha: float, mode: int = BUDGET_PROP
                       -> w_i = (1 - alpha) n_i / M + alpha S_i / S
         raw:          r_i = r_base + alpha (Ibar_i - Ibar_avg)
                       -> w_i = n_i / M + alpha (S_i - n_i S / M) / K
-    Negative w are clamped to 0; W_i = max(1, rint(w_i 2^28)) so that every
+    Negative w are clamped to 0 and w above 64 to 64 (keeps the integer
+    stage within 63-bit products); W_i = max(1, rint(w_i 2^28)) so that every
     image stays in the water-filling.  If S is not positive and finite, every
     image gets its token share n_i / M.  Each operation is one IEEE float64
     operation, evaluated left to right, no fused multiply-add.
@@ -259,6 +261,8 @@ def budget_weights(n_list, S_list, K: int, alpha: float, mode: int = BUDGET_PROP
             w = u + alpha * ((s - u * S) / float(K)) if K > 0 else u
         if not (w > 0.0):
             w = 0.0
+        if w > WEIGHT_CAP:
+            w = WEIGHT_CAP
         W.append(max(1, int(round(w * float(1 << WEIGHT_BITS)))))
     return W
 

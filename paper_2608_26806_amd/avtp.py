@@ -1,0 +1,291 @@
+"""ctypes binding of libavtp.so (argument marshalling only).
+
+Every step of the pruning layer runs in the library's HIP kernels; this module
+turns torch tensors into device pointers, passes torch's current HIP stream,
+and raises ``AvtpError`` on a non-zero status.  There is no fallback: if the
+library is missing, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libavtp.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "avtp.h")
+
+BF16, FP32 = 0, 1
+SCORE_ATTN, SCORE_VARIATION = 0, 1
+BUDGET_PROPORTIONAL, BUDGET_RAW = 0, 1
+FLAG_NAN_SCORE, FLAG_NO_TEXT_AFTER, FLAG_INFEASIBLE, FLAG_OUT_CAPACITY = 1, 2, 4, 8
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_INFEASIBLE, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4, -5
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+
+
+class _Layout(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("n_img", ctypes.c_int32), ("N_tok", ctypes.c_int32),
+                ("T_tot", ctypes.c_int32)] + \
+               [(n, ctypes.c_void_p) for n in ("cu_seqlens", "img_start", "img_len", "cu_img",
+                                                "text_pos", "cu_text", "keep_total")] + \
+               [(n, ctypes.c_void_p) for n in ("h_cu_seqlens", "h_img_start", "h_img_len",
+                                                "h_cu_img", "h_text_pos", "h_cu_text",
+                                                "h_keep_total")]
+
+
+class _Tensor(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("row_bytes", ctypes.c_int64),
+                ("src_stride", ctypes.c_int64), ("dst_stride", ctypes.c_int64),
+                ("planes", ctypes.c_int32), ("src_plane_stride", ctypes.c_int64),
+                ("dst_plane_stride", ctypes.c_int64)]
+
+
+class AvtpError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {status_string(code)} ({code})")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libavtp.so (raises if it was not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing; build it with "
+                               "`python -m paper_2608_26806_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, c_int, c_float, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        LP = ctypes.POINTER(_Layout)
+        L.avtp_score_workspace_size.argtypes = [LP, c_int, c_int, c_int, c_int, c_int]
+        L.avtp_score_workspace_size.restype = sz
+        L.avtp_score.argtypes = [vp, LP, c_int, c_int, vp, vp, c_int, c_int, c_int, c_float, vp, vp,
+                                 vp, c_int, vp, vp, vp, vp, sz]
+        L.avtp_row_lse.argtypes = [vp, LP, c_int, vp, vp, c_int, c_int, c_int, c_float, vp, vp, sz]
+        L.avtp_budget.argtypes = [vp, LP, vp, c_int, c_float, c_int, c_int, c_int, vp, vp]
+        L.avtp_select.argtypes = [vp, LP, vp, vp, vp, ctypes.c_int64, vp, vp]
+        L.avtp_compact.argtypes = [vp, LP, vp, ctypes.c_int64, ctypes.POINTER(_Tensor), c_int]
+        L.avtp_status_string.argtypes = [c_int]
+        L.avtp_status_string.restype = ctypes.c_char_p
+        L.avtp_version.restype = c_int
+        for f in ("avtp_score", "avtp_row_lse", "avtp_budget", "avtp_select", "avtp_compact"):
+            getattr(L, f).restype = c_int
+        _lib = L
+    return _lib
+
+
+def header_functions() -> list:
+    """Names of the functions include/avtp.h declares."""
+    text = open(HEADER_PATH).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(avtp_[a-z_]+)\s*\(", text)))
+
+
+def status_string(code: int) -> str:
+    return lib().avtp_status_string(int(code)).decode()
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != OK:
+        raise AvtpError(rc, where)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return FP32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+class DeviceLayout:
+    """A packed batch layout with device arrays and their host mirrors.
+
+    ``arrays`` maps cu_seqlens, img_start, img_len, cu_img, text_pos, cu_text,
+    keep_total to int32 sequences (an object with those attributes works too).
+    """
+
+    NAMES = ("cu_seqlens", "img_start", "img_len", "cu_img", "text_pos", "cu_text", "keep_total")
+
+    def __init__(self, arrays, device="cuda", host_only: bool = False):
+        get = (lambda n: arrays[n]) if isinstance(arrays, dict) else (lambda n: getattr(arrays, n))
+        self.host = {n: np.ascontiguousarray(np.asarray(get(n), dtype=np.int32)) for n in self.NAMES}
+        h = self.host
+        self.B = len(h["cu_seqlens"]) - 1
+        self.n_img = len(h["img_len"])
+        self.N_tok = int(h["cu_seqlens"][-1]) if self.B >= 0 and len(h["cu_seqlens"]) else 0
+        self.T_tot = len(h["text_pos"])
+        self.N_out = int(self.T_tot + int(np.sum(h["keep_total"], dtype=np.int64)))
+        # one device buffer holds every array (a zero-length array still gets a valid pointer)
+        offs, tot = {}, 0
+        for n in self.NAMES:
+            offs[n] = tot
+            tot += max(1, len(h[n]))
+        flat = np.zeros(tot, dtype=np.int32)
+        for n in self.NAMES:
+            flat[offs[n]:offs[n] + len(h[n])] = h[n]
+        if host_only:
+            self.dev = torch.from_numpy(flat)
+        else:
+            self.dev = torch.from_numpy(flat).to(device)
+        base, es = self.dev.data_ptr(), 4
+        self.st = _Layout(self.B, self.n_img, self.N_tok, self.T_tot,
+                          *[base + es * offs[n] for n in self.NAMES],
+                          *[h[n].ctypes.data for n in self.NAMES])
+
+    def ref(self):
+        return ctypes.byref(self.st)
+
+    def device_array(self, name: str) -> torch.Tensor:
+        h = self.host[name]
+        off = self.st.__getattribute__(name) - self.dev.data_ptr()
+        return self.dev[off // 4: off // 4 + len(h)]
+
+
+# --------------------------------------------------------------------------- score
+def score_workspace_bytes(dl: DeviceLayout, mode: int, dtype: int = BF16, Hq: int = 1,
+                          Hkv: int = 1, d: int = 128) -> int:
+    return int(lib().avtp_score_workspace_size(dl.ref(), mode, dtype, Hq, Hkv, d))
+
+
+def alloc_workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(1, nbytes), dtype=torch.uint8, device=device)
+
+
+def row_lse(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor, softmax_scale: float,
+            out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+            stream=None) -> torch.Tensor:
+    T, Hq, d = q_text.shape
+    Hkv = k.shape[1]
+    dt = dtype_code(q_text)
+    if out is None:
+        out = torch.empty((Hq, T), dtype=torch.float32, device=q_text.device)
+    if ws is None:
+        ws = alloc_workspace(score_workspace_bytes(dl, SCORE_ATTN, dt, Hq, Hkv, d), q_text.device)
+    _check(lib().avtp_row_lse(_stream(stream), dl.ref(), dt, _ptr(q_text), _ptr(k), Hq, Hkv, d,
+                              float(softmax_scale), _ptr(out), _ptr(ws), ws.numel()), "avtp_row_lse")
+    return out
+
+
+def score_attn(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor, softmax_scale: float,
+               row_lse: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
+               img_sum: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
+               ws: Optional[torch.Tensor] = None, stream=None):
+    T, Hq, d = q_text.shape
+    Hkv = k.shape[1]
+    dt = dtype_code(q_text)
+    dev = q_text.device
+    if scores is None:
+        scores = torch.empty(dl.N_tok, dtype=torch.float32, device=dev)
+    if img_sum is None:
+        img_sum = torch.empty(max(1, dl.n_img), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = alloc_workspace(score_workspace_bytes(dl, SCORE_ATTN, dt, Hq, Hkv, d), dev)
+    _check(lib().avtp_score(_stream(stream), dl.ref(), SCORE_ATTN, dt, _ptr(q_text), _ptr(k), Hq,
+                            Hkv, d, float(softmax_scale), _ptr(row_lse), None, None, 0,
+                            _ptr(scores), _ptr(img_sum), _ptr(status), _ptr(ws), ws.numel()),
+           "avtp_score")
+    return scores, img_sum[: dl.n_img]
+
+
+def score_variation(dl: DeviceLayout, h_cur: torch.Tensor, h_prior: torch.Tensor,
+                    scores: Optional[torch.Tensor] = None, img_sum: Optional[torch.Tensor] = None,
+                    status: Optional[torch.Tensor] = None, stream=None):
+    dev = h_cur.device
+    hidden = h_cur.shape[-1]
+    if scores is None:
+        scores = torch.empty(dl.N_tok, dtype=torch.float32, device=dev)
+    if img_sum is None:
+        img_sum = torch.empty(max(1, dl.n_img), dtype=torch.float32, device=dev)
+    ws = alloc_workspace(score_workspace_bytes(dl, SCORE_VARIATION), dev)
+    _check(lib().avtp_score(_stream(stream), dl.ref(), SCORE_VARIATION, dtype_code(h_cur), None,
+                            None, 0, 0, 0, 1.0, None, _ptr(h_cur), _ptr(h_prior), hidden,
+                            _ptr(scores), _ptr(img_sum), _ptr(status), _ptr(ws), ws.numel()),
+           "avtp_score")
+    return scores, img_sum[: dl.n_img]
+
+
+# --------------------------------------------------------------------------- budget
+def budget(dl: DeviceLayout, img_sum: torch.Tensor, alpha: float = 1.0, lo_permille: int = 50,
+           hi_permille: int = 950, floor_abs: int = 0, mode: int = BUDGET_PROPORTIONAL,
+           out: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
+           stream=None) -> torch.Tensor:
+    if out is None:
+        out = torch.empty(max(1, dl.n_img), dtype=torch.int32, device=img_sum.device)
+    _check(lib().avtp_budget(_stream(stream), dl.ref(), _ptr(img_sum), mode, float(alpha),
+                             lo_permille, hi_permille, floor_abs, _ptr(out), _ptr(status)),
+           "avtp_budget")
+    return out[: dl.n_img]
+
+
+# --------------------------------------------------------------------------- select
+def select(dl: DeviceLayout, scores: torch.Tensor, budget_: torch.Tensor,
+           keep_idx: Optional[torch.Tensor] = None, cu_out: Optional[torch.Tensor] = None,
+           status: Optional[torch.Tensor] = None, stream=None):
+    dev = scores.device
+    if keep_idx is None:
+        keep_idx = torch.empty(max(1, dl.N_out), dtype=torch.int32, device=dev)
+    if cu_out is None:
+        cu_out = torch.empty(dl.B + 1, dtype=torch.int32, device=dev)
+    _check(lib().avtp_select(_stream(stream), dl.ref(), _ptr(scores), _ptr(budget_),
+                             _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out), _ptr(status)),
+           "avtp_select")
+    return keep_idx[: dl.N_out], cu_out
+
+
+# --------------------------------------------------------------------------- compact
+def tensor_desc(src: torch.Tensor, dst: torch.Tensor, token_dim: int = 0) -> _Tensor:
+    """Descriptor of a gather along ``token_dim`` (0: [N, ...]; 1: [P, N, ...])."""
+    es = src.element_size()
+    if token_dim == 0:
+        row = src[0]
+        if not row.is_contiguous() or not dst[0].is_contiguous():
+            raise ValueError("rows must be contiguous")
+        return _Tensor(src.data_ptr(), dst.data_ptr(), row.numel() * es, src.stride(0) * es,
+                       dst.stride(0) * es, 1, 0, 0)
+    if token_dim == 1:
+        row = src[0, 0]
+        if not row.is_contiguous() or not dst[0, 0].is_contiguous():
+            raise ValueError("rows must be contiguous")
+        return _Tensor(src.data_ptr(), dst.data_ptr(), row.numel() * es, src.stride(1) * es,
+                       dst.stride(1) * es, src.shape[0], src.stride(0) * es, dst.stride(0) * es)
+    raise ValueError("token_dim must be 0 or 1")
+
+
+def compact(dl: DeviceLayout, keep_idx: torch.Tensor, pairs: Sequence, n_out: Optional[int] = None,
+            stream=None) -> None:
+    """pairs: (src, dst) or (src, dst, token_dim) tuples; dst is written in place."""
+    descs = [tensor_desc(p[0], p[1], p[2] if len(p) > 2 else 0) for p in pairs]
+    arr = (_Tensor * max(1, len(descs)))(*descs)
+    n = dl.N_out if n_out is None else int(n_out)
+    _check(lib().avtp_compact(_stream(stream), dl.ref(), _ptr(keep_idx), n, arr, len(descs)),
+           "avtp_compact")
+
+
+def compact_new(dl: DeviceLayout, keep_idx: torch.Tensor, srcs: Sequence, stream=None):
+    """Allocate outputs and compact (src, token_dim) pairs; returns the outputs."""
+    outs, pairs = [], []
+    for src, tdim in srcs:
+        shape = list(src.shape)
+        shape[tdim] = dl.N_out
+        dst = torch.empty(shape, dtype=src.dtype, device=src.device)
+        outs.append(dst)
+        pairs.append((src, dst, tdim))
+    compact(dl, keep_idx, pairs, stream=stream)
+    return outs

@@ -1,0 +1,240 @@
+// Host layer of libavtp.so: argument validation (pure host code, runs before
+// any HIP call and therefore also without a GPU), workspace sizing and the
+// C entry points declared in include/avtp.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+
+#include "avtp_internal.h"
+
+namespace avtp {
+namespace {
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? AVTP_OK : AVTP_ERR_HIP; }
+
+// Validate the packed layout from its host mirrors and derive launch maxima.
+// Checks: array presence; monotone offsets; images ascending, non-overlapping,
+// inside their sequence; text ascending and inside the sequence; every token
+// is text or visual (the lengths partition each sequence); size limits.
+int check_layout(const avtp_layout *lay, DevLayout *out) {
+  if (!lay) return AVTP_ERR_INVALID_ARG;
+  const int B = lay->B, n_img = lay->n_img, N = lay->N_tok, T = lay->T_tot;
+  if (B < 1 || n_img < 0 || N < 1 || T < 0) return AVTP_ERR_INVALID_ARG;
+  if (!lay->cu_seqlens || !lay->img_start || !lay->img_len || !lay->cu_img || !lay->text_pos ||
+      !lay->cu_text || !lay->keep_total)
+    return AVTP_ERR_INVALID_ARG;
+  if (!lay->h_cu_seqlens || !lay->h_img_start || !lay->h_img_len || !lay->h_cu_img ||
+      !lay->h_text_pos || !lay->h_cu_text || !lay->h_keep_total)
+    return AVTP_ERR_INVALID_ARG;
+  if (n_img > AVTP_MAX_IMAGES) return AVTP_ERR_UNSUPPORTED;
+  const int32_t *cs = lay->h_cu_seqlens, *ci = lay->h_cu_img, *ct = lay->h_cu_text;
+  if (cs[0] != 0 || ci[0] != 0 || ct[0] != 0) return AVTP_ERR_INVALID_ARG;
+  if (cs[B] != N || ci[B] != n_img || ct[B] != T) return AVTP_ERR_INVALID_ARG;
+  int max_seq = 0, max_text = 0, max_img = 0;
+  for (int b = 0; b < B; ++b) {
+    const int s0 = cs[b], s1 = cs[b + 1];
+    if (s1 < s0 || ci[b + 1] < ci[b] || ct[b + 1] < ct[b]) return AVTP_ERR_INVALID_ARG;
+    if (ci[b + 1] - ci[b] > AVTP_MAX_IMAGES_PER_SEQ) return AVTP_ERR_UNSUPPORTED;
+    int64_t covered = ct[b + 1] - ct[b];
+    int prev_end = s0;
+    for (int i = ci[b]; i < ci[b + 1]; ++i) {
+      const int st = lay->h_img_start[i], n = lay->h_img_len[i];
+      if (n < 0 || st < prev_end || (int64_t)st + n > s1) return AVTP_ERR_INVALID_ARG;
+      if (n > AVTP_MAX_IMAGE_LEN) return AVTP_ERR_UNSUPPORTED;
+      prev_end = st + n;
+      covered += n;
+      max_img = std::max(max_img, n);
+    }
+    if (covered != s1 - s0) return AVTP_ERR_INVALID_ARG;
+    // text rows: ascending, inside the sequence, outside every image (merge walk)
+    int img = ci[b], prev = s0 - 1;
+    for (int t = ct[b]; t < ct[b + 1]; ++t) {
+      const int p = lay->h_text_pos[t];
+      if (p <= prev || p >= s1) return AVTP_ERR_INVALID_ARG;
+      while (img < ci[b + 1] && lay->h_img_start[img] + lay->h_img_len[img] <= p) ++img;
+      if (img < ci[b + 1] && lay->h_img_start[img] <= p) return AVTP_ERR_INVALID_ARG;
+      prev = p;
+    }
+    if (lay->h_keep_total[b] < 0) return AVTP_ERR_INVALID_ARG;
+    max_seq = std::max(max_seq, s1 - s0);
+    max_text = std::max(max_text, ct[b + 1] - ct[b]);
+  }
+  if (out) {
+    *out = DevLayout{B, n_img, N, T, max_seq, max_text, max_img, lay->cu_seqlens, lay->img_start,
+                     lay->img_len, lay->cu_img, lay->text_pos, lay->cu_text, lay->keep_total};
+  }
+  return AVTP_OK;
+}
+
+int check_attn_args(int dtype, int Hq, int Hkv, int d) {
+  if (dtype != AVTP_BF16 && dtype != AVTP_FP32) return AVTP_ERR_UNSUPPORTED;
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return AVTP_ERR_INVALID_ARG;
+  if (d != 64 && d != 128) return AVTP_ERR_UNSUPPORTED;
+  if (Hq > 256) return AVTP_ERR_UNSUPPORTED;
+  return AVTP_OK;
+}
+
+int64_t n_out_of(const avtp_layout *lay) {
+  int64_t n = lay->T_tot;
+  for (int b = 0; b < lay->B; ++b) n += lay->h_keep_total[b];
+  return n;
+}
+
+}  // namespace
+}  // namespace avtp
+
+using namespace avtp;
+
+extern "C" {
+
+int avtp_version(void) { return (1 << 16) | 0; }
+
+const char *avtp_status_string(int s) {
+  switch (s) {
+    case AVTP_OK: return "AVTP_OK";
+    case AVTP_ERR_INVALID_ARG: return "AVTP_ERR_INVALID_ARG: invalid argument or layout";
+    case AVTP_ERR_UNSUPPORTED: return "AVTP_ERR_UNSUPPORTED: unsupported dtype, head_dim or size";
+    case AVTP_ERR_INFEASIBLE: return "AVTP_ERR_INFEASIBLE: keep_total outside the per-image bounds";
+    case AVTP_ERR_WORKSPACE: return "AVTP_ERR_WORKSPACE: workspace missing or too small";
+    case AVTP_ERR_HIP: return "AVTP_ERR_HIP: a HIP launch failed";
+    default: return "unknown avtp status";
+  }
+}
+
+size_t avtp_score_workspace_size(const avtp_layout *layout, int mode, int dtype, int Hq, int Hkv,
+                                 int d) {
+  DevLayout L;
+  if (check_layout(layout, &L) != AVTP_OK) return 0;
+  if (mode == AVTP_SCORE_VARIATION) return variation_workspace_bytes(L);
+  if (mode != AVTP_SCORE_ATTN || check_attn_args(dtype, Hq, Hkv, d) != AVTP_OK) return 0;
+  return attn_plan(L, Hq, Hkv, d, dtype).bytes;
+}
+
+int avtp_row_lse(avtp_stream_t stream, const avtp_layout *layout, int dtype, const void *q_text,
+                 const void *k, int Hq, int Hkv, int d, float softmax_scale, float *row_lse_out,
+                 void *ws, size_t ws_bytes) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  if ((rc = check_attn_args(dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
+  if (!q_text || !k || !row_lse_out || !(std::isfinite(softmax_scale)) || softmax_scale <= 0.f)
+    return AVTP_ERR_INVALID_ARG;
+  if ((uintptr_t)q_text % 16 || (uintptr_t)k % 16) return AVTP_ERR_INVALID_ARG;
+  AttnPlan P = attn_plan(L, Hq, Hkv, d, dtype);
+  if (!ws || ws_bytes < P.bytes || (uintptr_t)ws % 256) return AVTP_ERR_WORKSPACE;
+  if (L.T_tot == 0) return AVTP_OK;
+  return hip_status(launch_row_lse((hipStream_t)stream, L, P, dtype, q_text, k, Hq, Hkv, d,
+                                   softmax_scale, row_lse_out, (char *)ws));
+}
+
+int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dtype,
+               const void *q_text, const void *k, int Hq, int Hkv, int d, float softmax_scale,
+               const float *row_lse, const void *h_cur, const void *h_prior, int hidden,
+               float *scores, float *img_sum, int32_t *status, void *ws, size_t ws_bytes) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  if (!scores || (L.n_img > 0 && !img_sum)) return AVTP_ERR_INVALID_ARG;
+  hipStream_t st = (hipStream_t)stream;
+  if (mode == AVTP_SCORE_VARIATION) {
+    if (dtype != AVTP_BF16 && dtype != AVTP_FP32) return AVTP_ERR_UNSUPPORTED;
+    if (!h_cur || !h_prior || hidden < 1) return AVTP_ERR_INVALID_ARG;
+    if (hidden % 8 != 0) return AVTP_ERR_UNSUPPORTED;
+    if ((uintptr_t)h_cur % 16 || (uintptr_t)h_prior % 16) return AVTP_ERR_INVALID_ARG;
+    if (ws_bytes < variation_workspace_bytes(L)) return AVTP_ERR_WORKSPACE;
+    hipError_t e = launch_variation(st, L, dtype, h_cur, h_prior, hidden, scores);
+    if (e == hipSuccess) e = launch_finalize(st, L, nullptr, 0, 0, scores, img_sum, status);
+    return hip_status(e);
+  }
+  if (mode != AVTP_SCORE_ATTN) return AVTP_ERR_INVALID_ARG;
+  if ((rc = check_attn_args(dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
+  if (!q_text || !k || !(std::isfinite(softmax_scale)) || softmax_scale <= 0.f)
+    return AVTP_ERR_INVALID_ARG;
+  if ((uintptr_t)q_text % 16 || (uintptr_t)k % 16 || (row_lse && (uintptr_t)row_lse % 4))
+    return AVTP_ERR_INVALID_ARG;
+  AttnPlan P = attn_plan(L, Hq, Hkv, d, dtype);
+  if (!ws || ws_bytes < P.bytes || (uintptr_t)ws % 256) return AVTP_ERR_WORKSPACE;
+  char *w = (char *)ws;
+  hipError_t e = hipSuccess;
+  const float *lse = row_lse;
+  if (!lse) {
+    float *own = (float *)(w + P.off_lse);
+    if (L.T_tot > 0)
+      e = launch_row_lse(st, L, P, dtype, q_text, k, Hq, Hkv, d, softmax_scale, own, w);
+    lse = own;
+  }
+  if (e == hipSuccess && L.T_tot > 0)
+    e = launch_colsum(st, L, P, dtype, q_text, k, Hq, Hkv, d, softmax_scale, lse, w);
+  if (e == hipSuccess)
+    e = launch_finalize(st, L, (const float *)(w + P.off_colsum), Hq, Hkv, scores, img_sum,
+                        status);
+  return hip_status(e);
+}
+
+int avtp_budget(avtp_stream_t stream, const avtp_layout *layout, const float *img_sum, int mode,
+                float alpha, int lo_permille, int hi_permille, int floor_abs, int32_t *budget,
+                int32_t *status) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  if (mode != AVTP_BUDGET_PROPORTIONAL && mode != AVTP_BUDGET_RAW) return AVTP_ERR_INVALID_ARG;
+  if (!(alpha >= 0.f && alpha <= 32.f)) return AVTP_ERR_INVALID_ARG;
+  if (lo_permille < 0 || hi_permille > 1000 || lo_permille > hi_permille || floor_abs < 0)
+    return AVTP_ERR_INVALID_ARG;
+  if (L.n_img > 0 && (!img_sum || !budget)) return AVTP_ERR_INVALID_ARG;
+  // feasibility: sum lo <= keep_total <= sum hi for every sequence
+  for (int b = 0; b < L.B; ++b) {
+    int64_t slo = 0, shi = 0;
+    for (int i = layout->h_cu_img[b]; i < layout->h_cu_img[b + 1]; ++i) {
+      const int64_t n = layout->h_img_len[i];
+      const int64_t lo = std::min<int64_t>(n, std::max<int64_t>((lo_permille * n + 999) / 1000, floor_abs));
+      const int64_t hi = std::max<int64_t>(lo, (hi_permille * n) / 1000);
+      slo += lo;
+      shi += hi;
+    }
+    const int64_t K = layout->h_keep_total[b];
+    if (K < slo || K > shi) return AVTP_ERR_INFEASIBLE;
+  }
+  if (L.n_img == 0) return AVTP_OK;
+  return hip_status(launch_budget((hipStream_t)stream, L, img_sum, mode, alpha, lo_permille,
+                                  hi_permille, floor_abs, budget, status));
+}
+
+int avtp_select(avtp_stream_t stream, const avtp_layout *layout, const float *scores,
+                const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out,
+                int32_t *status) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  if (!scores || !cu_out || (L.n_img > 0 && !budget)) return AVTP_ERR_INVALID_ARG;
+  const int64_t need = n_out_of(layout);
+  if (keep_capacity < need || (need > 0 && !keep_idx)) return AVTP_ERR_INVALID_ARG;
+  return hip_status(launch_select((hipStream_t)stream, L, scores, budget, keep_idx,
+                                  keep_capacity, cu_out, status));
+}
+
+int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,
+                 int64_t n_out, const avtp_tensor *tensors, int n_tensors) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  if (n_tensors < 0 || n_out < 0) return AVTP_ERR_INVALID_ARG;
+  if (n_tensors > AVTP_MAX_TENSORS) return AVTP_ERR_UNSUPPORTED;
+  if (n_tensors > 0 && !tensors) return AVTP_ERR_INVALID_ARG;
+  if (n_out > 0 && !keep_idx) return AVTP_ERR_INVALID_ARG;
+  if (n_out > n_out_of(layout)) return AVTP_ERR_INVALID_ARG;
+  for (int i = 0; i < n_tensors; ++i) {
+    const avtp_tensor &t = tensors[i];
+    if (!t.src || !t.dst || t.row_bytes < 1 || t.planes < 1) return AVTP_ERR_INVALID_ARG;
+    if (t.src_stride < t.row_bytes || t.dst_stride < t.row_bytes) return AVTP_ERR_INVALID_ARG;
+    if (t.planes > 1 && (t.src_plane_stride < (int64_t)L.N_tok * t.src_stride ||
+                         t.dst_plane_stride < n_out * t.dst_stride))
+      return AVTP_ERR_INVALID_ARG;
+  }
+  if (n_out == 0 || n_tensors == 0) return AVTP_OK;
+  return hip_status(launch_compact((hipStream_t)stream, L, keep_idx, n_out, tensors, n_tensors));
+}
+
+}  // extern "C"

@@ -1,0 +1,57 @@
+// Internal interface between the host layer (avtp_api.cpp) and the HIP
+// kernels.  Every launcher enqueues on `stream` and returns the hipError_t of
+// its launches; all arguments were validated by the host layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/avtp.h"
+
+namespace avtp {
+
+// Device view of a validated layout (device pointers plus host-derived maxima).
+struct DevLayout {
+  int B, n_img, N_tok, T_tot;
+  int max_seqlen, max_text, max_img_len;
+  const int32_t *cu_seqlens, *img_start, *img_len, *cu_img, *text_pos, *cu_text, *keep_total;
+};
+
+// Launch geometry of the two attention passes, derived from the layout only
+// (so the workspace size and the launches always agree).
+struct AttnPlan {
+  int G;          // query heads per key head
+  int rows_max;   // max over sequences of G * T_b
+  int nqb;        // query blocks per (sequence, key head) in pass 1
+  int kchunk;     // keys per pass-1 chunk (multiple of 64)
+  int nkc;        // chunks per sequence (max)
+  int nkb;        // key blocks per (sequence, key head) in pass 2
+  size_t off_part_m, off_part_l, off_lse, off_colsum, bytes;
+};
+
+AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype);
+size_t variation_workspace_bytes(const DevLayout &L);
+
+hipError_t launch_row_lse(hipStream_t stream, const DevLayout &L, const AttnPlan &P, int dtype,
+                          const void *q, const void *k, int Hq, int Hkv, int d, float scale,
+                          float *row_lse, char *ws);
+hipError_t launch_colsum(hipStream_t stream, const DevLayout &L, const AttnPlan &P, int dtype,
+                         const void *q, const void *k, int Hq, int Hkv, int d, float scale,
+                         const float *row_lse, char *ws);
+// Per-image finalisation shared by both score modes.  colsum == nullptr:
+// scores already hold the per-token values (variation mode).
+hipError_t launch_finalize(hipStream_t stream, const DevLayout &L, const float *colsum, int Hq,
+                           int Hkv, float *scores, float *img_sum, int32_t *status);
+hipError_t launch_variation(hipStream_t stream, const DevLayout &L, int dtype, const void *h_cur,
+                            const void *h_prior, int hidden, float *scores);
+hipError_t launch_budget(hipStream_t stream, const DevLayout &L, const float *img_sum, int mode,
+                         float alpha, int lo_permille, int hi_permille, int floor_abs,
+                         int32_t *budget, int32_t *status);
+hipError_t launch_select(hipStream_t stream, const DevLayout &L, const float *scores,
+                         const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
+                         int32_t *cu_out, int32_t *status);
+hipError_t launch_compact(hipStream_t stream, const DevLayout &L, const int32_t *keep_idx,
+                          int64_t n_out, const avtp_tensor *tensors, int n_tensors);
+
+}  // namespace avtp

@@ -1,0 +1,137 @@
+// Stable compaction out[r] = in[keep_idx[r]] of up to AVTP_MAX_TENSORS
+// tensors in one launch (the shortened sequence that continues through the
+// layers after pruning; position ids keep their original values).
+//
+// HBM-bound bit copy.  Each tensor gets its own range of blocks; a block
+// copies a run of output rows of one plane.  Rows are split into the widest
+// aligned vector unit (16 bytes where possible); a power-of-two group of
+// lanes covers one row, so small rows (position ids, per-head K/V rows) pack
+// several rows per wave and large rows (hidden states) use the whole block.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "avtp_internal.h"
+
+namespace avtp {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kBlockBytes = 32768;  // target bytes per block
+
+struct CTensor {
+  const char *src;
+  char *dst;
+  long long src_stride, dst_stride, src_plane_stride, dst_plane_stride;
+  int units;       // vector units per row
+  int vshift;      // log2 of the vector width in bytes
+  int lpr_shift;   // log2 of lanes per row
+  int planes;
+  int rows_per_block;
+  int blocks_per_plane;
+  int block_begin;
+};
+
+struct CArgs {
+  CTensor t[AVTP_MAX_TENSORS];
+  int n;
+  const int32_t *keep_idx;
+  long long n_out;
+  int N_tok;
+};
+
+template <typename V>
+__device__ inline void copy_rows(const CTensor &T, const int32_t *__restrict__ keep_idx,
+                                 long long r0, long long r1, int N_tok, int plane) {
+  const int tid = threadIdx.x;
+  const int lpr = 1 << T.lpr_shift;
+  const int lane = tid & (lpr - 1);
+  const int rows_per_pass = kThreads >> T.lpr_shift;
+  const char *src = T.src + plane * T.src_plane_stride;
+  char *dst = T.dst + plane * T.dst_plane_stride;
+  for (long long r = r0 + (tid >> T.lpr_shift); r < r1; r += rows_per_pass) {
+    const int j = keep_idx[r];
+    if ((unsigned)j >= (unsigned)N_tok) continue;  // out-of-range index: row left untouched
+    const V *s = reinterpret_cast<const V *>(src + (long long)j * T.src_stride);
+    V *d = reinterpret_cast<V *>(dst + r * T.dst_stride);
+    int u = lane;
+    for (; u + lpr < T.units; u += 2 * lpr) {  // two independent loads in flight
+      const V a = s[u], b = s[u + lpr];
+      d[u] = a;
+      d[u + lpr] = b;
+    }
+    if (u < T.units) d[u] = s[u];
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void compact_kernel(CArgs a) {
+  int ti = 0;
+  while (ti + 1 < a.n && (int)blockIdx.x >= a.t[ti + 1].block_begin) ++ti;
+  const CTensor &T = a.t[ti];
+  const int local = blockIdx.x - T.block_begin;
+  const int plane = local / T.blocks_per_plane;
+  const int rb = local - plane * T.blocks_per_plane;
+  const long long r0 = (long long)rb * T.rows_per_block;
+  long long r1 = r0 + T.rows_per_block;
+  if (r1 > a.n_out) r1 = a.n_out;
+  switch (T.vshift) {
+    case 4: copy_rows<uint4>(T, a.keep_idx, r0, r1, a.N_tok, plane); break;
+    case 3: copy_rows<uint2>(T, a.keep_idx, r0, r1, a.N_tok, plane); break;
+    case 2: copy_rows<uint32_t>(T, a.keep_idx, r0, r1, a.N_tok, plane); break;
+    case 1: copy_rows<uint16_t>(T, a.keep_idx, r0, r1, a.N_tok, plane); break;
+    default: copy_rows<uint8_t>(T, a.keep_idx, r0, r1, a.N_tok, plane); break;
+  }
+}
+
+int ilog2(long long v) {
+  int s = 0;
+  while ((1ll << (s + 1)) <= v) ++s;
+  return s;
+}
+
+}  // namespace
+
+hipError_t launch_compact(hipStream_t st, const DevLayout &L, const int32_t *keep_idx,
+                          int64_t n_out, const avtp_tensor *tensors, int n_tensors) {
+  CArgs a;
+  a.n = n_tensors;
+  a.keep_idx = keep_idx;
+  a.n_out = n_out;
+  a.N_tok = L.N_tok;
+  long long blocks = 0;
+  for (int i = 0; i < n_tensors; ++i) {
+    const avtp_tensor &x = tensors[i];
+    long long v = 16;
+    auto misaligned = [&](long long m) {
+      return (x.row_bytes % m) || (x.src_stride % m) || (x.dst_stride % m) ||
+             ((uintptr_t)x.src % m) || ((uintptr_t)x.dst % m) ||
+             (x.planes > 1 && ((x.src_plane_stride % m) || (x.dst_plane_stride % m)));
+    };
+    while (v > 1 && misaligned(v)) v >>= 1;
+    CTensor &T = a.t[i];
+    T.src = (const char *)x.src;
+    T.dst = (char *)x.dst;
+    T.src_stride = x.src_stride;
+    T.dst_stride = x.dst_stride;
+    T.src_plane_stride = x.src_plane_stride;
+    T.dst_plane_stride = x.dst_plane_stride;
+    T.vshift = ilog2(v);
+    T.units = (int)(x.row_bytes / v);
+    long long lpr = 1;
+    while (lpr < T.units && lpr < kThreads) lpr <<= 1;
+    T.lpr_shift = ilog2(lpr);
+    const long long rows_per_pass = kThreads / lpr;
+    long long rpb = (kBlockBytes + x.row_bytes - 1) / x.row_bytes;
+    rpb = ((rpb + rows_per_pass - 1) / rows_per_pass) * rows_per_pass;
+    T.rows_per_block = (int)rpb;
+    T.blocks_per_plane = (int)((n_out + rpb - 1) / rpb);
+    T.planes = x.planes;
+    T.block_begin = (int)blocks;
+    blocks += (long long)T.blocks_per_plane * x.planes;
+  }
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(compact_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace avtp

@@ -1,0 +1,96 @@
+// Hidden-state-variation score (Sec. 3.3.1 of the paper): for visual token j
+//   I_j = 1 - <h_j, h'_j> / max(|h_j| |h'_j|, 1e-8)
+// with h the hidden state at the pruning layer and h' the state saved after
+// the previous pruning (the input embeddings before the first one).
+// HBM-bound: one wave streams both rows of a token with 16-byte loads and
+// reduces the three fp32 sums with a fixed butterfly.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "avtp_internal.h"
+
+namespace avtp {
+namespace {
+
+constexpr int kTokPerWave = 4;
+constexpr int kTokPerBlock = 4 * kTokPerWave;
+
+__device__ inline void acc8(const uint4 &x, const uint4 &y, float &dot, float &nx, float &ny,
+                            __bf16 *) {
+  const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, ys[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float x0 = __uint_as_float(xs[w] << 16), x1 = __uint_as_float(xs[w] & 0xffff0000u);
+    const float y0 = __uint_as_float(ys[w] << 16), y1 = __uint_as_float(ys[w] & 0xffff0000u);
+    dot += x0 * y0;
+    dot += x1 * y1;
+    nx += x0 * x0;
+    nx += x1 * x1;
+    ny += y0 * y0;
+    ny += y1 * y1;
+  }
+}
+__device__ inline void acc8(const uint4 &x, const uint4 &y, float &dot, float &nx, float &ny,
+                            float *) {
+  const float xs[4] = {__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z),
+                       __uint_as_float(x.w)};
+  const float ys[4] = {__uint_as_float(y.x), __uint_as_float(y.y), __uint_as_float(y.z),
+                       __uint_as_float(y.w)};
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    dot += xs[w] * ys[w];
+    nx += xs[w] * xs[w];
+    ny += ys[w] * ys[w];
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void variation_kernel(const char *__restrict__ hc,
+                                                        const char *__restrict__ hp, int hidden,
+                                                        const int32_t *__restrict__ img_start,
+                                                        const int32_t *__restrict__ img_len,
+                                                        float *__restrict__ scores) {
+  const int i = blockIdx.y;
+  const int n = img_len[i];
+  const int base = blockIdx.x * kTokPerBlock;
+  if (base >= n) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t row_bytes = (size_t)hidden * sizeof(T);
+  const int nvec = (int)(row_bytes / 16);
+  for (int tt = 0; tt < kTokPerWave; ++tt) {
+    const int tok = base + wave * kTokPerWave + tt;
+    if (tok >= n) break;
+    const size_t row = (size_t)img_start[i] + tok;
+    const uint4 *a = reinterpret_cast<const uint4 *>(hc + row * row_bytes);
+    const uint4 *b = reinterpret_cast<const uint4 *>(hp + row * row_bytes);
+    float dot = 0.f, nx = 0.f, ny = 0.f;
+    for (int v = lane; v < nvec; v += 64) acc8(a[v], b[v], dot, nx, ny, (T *)nullptr);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      dot += __shfl_xor(dot, off);
+      nx += __shfl_xor(nx, off);
+      ny += __shfl_xor(ny, off);
+    }
+    if (lane == 0) scores[row] = 1.f - dot / fmaxf(sqrtf(nx) * sqrtf(ny), 1e-8f);
+  }
+}
+
+}  // namespace
+
+size_t variation_workspace_bytes(const DevLayout &) { return 0; }
+
+hipError_t launch_variation(hipStream_t st, const DevLayout &L, int dtype, const void *h_cur,
+                            const void *h_prior, int hidden, float *scores) {
+  if (L.n_img == 0 || L.max_img_len == 0) return hipSuccess;
+  const dim3 grid((L.max_img_len + kTokPerBlock - 1) / kTokPerBlock, L.n_img);
+  if (dtype == AVTP_BF16)
+    hipLaunchKernelGGL(variation_kernel<__bf16>, grid, dim3(256), 0, st, (const char *)h_cur,
+                       (const char *)h_prior, hidden, L.img_start, L.img_len, scores);
+  else
+    hipLaunchKernelGGL(variation_kernel<float>, grid, dim3(256), 0, st, (const char *)h_cur,
+                       (const char *)h_prior, hidden, L.img_start, L.img_len, scores);
+  return hipGetLastError();
+}
+
+}  // namespace avtp

@@ -1,0 +1,138 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol, and
+rejects bad arguments on the host before anything is launched.
+
+Every call here fails validation, so no kernel is ever enqueued (there is no
+GPU in this test); the device pointers of the layout are host memory that the
+library never dereferences.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_26806_amd import avtp as A
+from paper_2608_26806_amd.workloads import build_layout
+
+
+def _dl(lay=None, **patch):
+    lay = lay or build_layout([[6, 4], [5]], 2, 3, 50)
+    arrays = {n: np.array(getattr(lay, n)) for n in A.DeviceLayout.NAMES}
+    arrays.update(patch)
+    return A.DeviceLayout(arrays, host_only=True)
+
+
+def _call_score(dl, d=128, Hq=4, Hkv=2, ws_bytes=None, dtype=A.BF16, scale=0.1):
+    buf = torch.zeros(1 << 16, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    n = buf.numel() if ws_bytes is None else ws_bytes
+    return A.lib().avtp_score(None, dl.ref(), A.SCORE_ATTN, dtype, p, p, Hq, Hkv, d, scale, None,
+                              None, None, 0, p, p, None, p, n)
+
+
+def test_exports_every_declared_function():
+    lib = A.lib()
+    names = A.header_functions()
+    assert {"avtp_score", "avtp_budget", "avtp_select", "avtp_compact"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.avtp_version() >> 16 == 1
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4, -5):
+        assert A.status_string(code).startswith("AVTP_")
+
+
+def test_null_layout_and_bad_offsets():
+    lib = A.lib()
+    buf = torch.zeros(64, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    assert lib.avtp_select(None, None, p, p, p, 100, p, None) == A.ERR_INVALID_ARG
+    bad = _dl(cu_seqlens=np.array([1, 17, 25]))
+    assert _call_score(bad) == A.ERR_INVALID_ARG
+
+
+def test_overlapping_images_rejected():
+    lay = build_layout([[6, 4]], 1, 2, 50)
+    st = np.array(lay.img_start)
+    st[1] = st[0] + 3                               # image 1 starts inside image 0
+    assert _call_score(_dl(lay, img_start=st)) == A.ERR_INVALID_ARG
+
+
+def test_text_inside_image_rejected():
+    lay = build_layout([[6, 4]], 1, 2, 50)
+    tp = np.array(lay.text_pos)
+    tp[0] = lay.img_start[0] + 1
+    tp.sort()
+    assert _call_score(_dl(lay, text_pos=tp)) == A.ERR_INVALID_ARG
+
+
+def test_uncovered_token_rejected():
+    lay = build_layout([[6, 4]], 1, 2, 50)
+    ln = np.array(lay.img_len)
+    ln[1] -= 1                                      # the last image token belongs to nothing
+    assert _call_score(_dl(lay, img_len=ln)) == A.ERR_INVALID_ARG
+
+
+def test_head_and_dtype_checks():
+    dl = _dl()
+    assert _call_score(dl, d=96) == A.ERR_UNSUPPORTED
+    assert _call_score(dl, Hq=6, Hkv=4) == A.ERR_INVALID_ARG
+    assert _call_score(dl, dtype=7) == A.ERR_UNSUPPORTED
+    assert _call_score(dl, scale=float("nan")) == A.ERR_INVALID_ARG
+
+
+def test_workspace_checks():
+    dl = _dl()
+    need = A.score_workspace_bytes(dl, A.SCORE_ATTN, A.BF16, 4, 2, 128)
+    assert need > 0
+    assert _call_score(dl, ws_bytes=need - 1) == A.ERR_WORKSPACE
+    bad = _dl(cu_seqlens=np.array([0, 5, 7]))
+    assert A.score_workspace_bytes(bad, A.SCORE_ATTN, A.BF16, 4, 2, 128) == 0
+
+
+def test_budget_infeasible_and_bad_alpha():
+    lay = build_layout([[20, 20]], 0, 1, 50)
+    buf = torch.zeros(64, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    lib = A.lib()
+    dl = _dl(lay, keep_total=np.array([39]))        # sum hi = 38 < 39
+    assert lib.avtp_budget(None, dl.ref(), p, 0, 1.0, 50, 950, 0, p, None) == A.ERR_INFEASIBLE
+    dl = _dl(lay, keep_total=np.array([10]))
+    assert lib.avtp_budget(None, dl.ref(), p, 0, 1.0, 50, 950, 8, p, None) == A.ERR_INFEASIBLE
+    assert lib.avtp_budget(None, dl.ref(), p, 0, -1.0, 50, 950, 0, p, None) == A.ERR_INVALID_ARG
+    assert lib.avtp_budget(None, dl.ref(), p, 0, 1.0, 600, 500, 0, p, None) == A.ERR_INVALID_ARG
+    assert lib.avtp_budget(None, dl.ref(), p, 5, 1.0, 50, 950, 0, p, None) == A.ERR_INVALID_ARG
+
+
+def test_select_capacity_checked():
+    dl = _dl()
+    buf = torch.zeros(64, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    assert A.lib().avtp_select(None, dl.ref(), p, p, p, dl.N_out - 1, p, None) == A.ERR_INVALID_ARG
+
+
+def test_compact_descriptor_checks():
+    dl = _dl()
+    src = torch.zeros((dl.N_tok, 8), dtype=torch.float32)
+    dst = torch.zeros((dl.N_out, 8), dtype=torch.float32)
+    keep = torch.zeros(dl.N_out, dtype=torch.int32)
+    lib = A.lib()
+    d = A.tensor_desc(src, dst)
+    arr = (A._Tensor * 9)(*([d] * 9))
+    assert lib.avtp_compact(None, dl.ref(), ctypes.c_void_p(keep.data_ptr()), dl.N_out, arr, 9) \
+        == A.ERR_UNSUPPORTED
+    d.src_stride = 4                                  # stride below the row size
+    arr = (A._Tensor * 1)(d)
+    assert lib.avtp_compact(None, dl.ref(), ctypes.c_void_p(keep.data_ptr()), dl.N_out, arr, 1) \
+        == A.ERR_INVALID_ARG
+    d = A.tensor_desc(src, dst)
+    arr = (A._Tensor * 1)(d)
+    assert lib.avtp_compact(None, dl.ref(), ctypes.c_void_p(keep.data_ptr()), dl.N_out + 1, arr, 1) \
+        == A.ERR_INVALID_ARG
+
+
+def test_layout_limits():
+    lay = build_layout([[1] * 257], 0, 1, 50)         # more images per sequence than supported
+    assert _call_score(_dl(lay)) == A.ERR_UNSUPPORTED

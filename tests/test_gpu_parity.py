@@ -1,0 +1,377 @@
+"""GPU parity: every call of libavtp.so against the CPU oracle, stage by stage
+and end to end, on the seeded workloads (small configurations in full,
+large ones on sampled outputs and invariants) and on edge cases.
+
+Tolerances: scores and image sums within 2e-3 relative for bf16 inputs and
+1e-5 for fp32 (rows of the LSE within the same bound, absolute, since an
+error e in lse scales every probability of the row by exp(e)); budgets,
+selections and compactions bit-exact given identical inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import (TOL, assert_rel, kept_sets_match, need_gpu, say, to_dev, to_host_bits)
+from oracle import avtp_oracle as O
+from paper_2608_26806_amd import avtp as A
+from paper_2608_26806_amd.workloads import (Layout, build_layout, duplicate_key_rows, f32_to_bf16_bits,
+                                            make_workload)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    need_gpu()
+    A.lib()
+
+
+_WL = {}
+
+
+def workload(cfg, **kw):
+    key = (cfg, tuple(sorted(kw.items())))
+    if key not in _WL:
+        _WL[key] = make_workload(cfg, **kw)
+    return _WL[key]
+
+
+def gpu_score(wl, dl):
+    q = to_dev(wl.q_text, wl.dtype)
+    k = to_dev(wl.k, wl.dtype)
+    lse = A.row_lse(dl, q, k, wl.softmax_scale)
+    status = torch.zeros(dl.B, dtype=torch.int32, device="cuda")
+    scores, isum = A.score_attn(dl, q, k, wl.softmax_scale, status=status)
+    torch.cuda.synchronize()
+    return (lse.cpu().numpy().astype(np.float64), scores.cpu().numpy(), isum.cpu().numpy(),
+            status.cpu().numpy())
+
+
+# ------------------------------------------------------------------ score: full oracle
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_score_parity_full(cfg):
+    wl = workload(cfg, payload=False)
+    lay = wl.layout
+    say(f"[score parity] config {cfg}: B={lay.B} N_tok={lay.N_tok} T={lay.T_tot} {wl.dtype}")
+    dl = A.DeviceLayout(lay)
+    lse_g, s_g, isum_g, status = gpu_score(wl, dl)
+    s_o, isum_o, lse_o, empty = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale,
+                                              wl.dtype, exact_dot=(cfg == 1))
+    tol = TOL[wl.dtype]
+    assert_rel(lse_g, lse_o, 0.0, "row lse", abs_floor=tol)
+    vis = lay.visual_mask()
+    assert_rel(s_g[vis], s_o[vis], tol, "scores")
+    assert np.all(np.isinf(s_g[~vis])) and np.all(s_g[~vis] > 0)
+    assert_rel(isum_g, isum_o, tol, "image sums")
+    assert not empty and not status.any()
+
+
+def test_score_with_supplied_lse_skips_pass1():
+    """Feeding the oracle's LSE (as the layer's own attention would) gives the same scores."""
+    wl = workload(2, payload=False)
+    lay = wl.layout
+    dl = A.DeviceLayout(lay)
+    s_o, isum_o, lse_o, _ = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale,
+                                          wl.dtype)
+    q, k = to_dev(wl.q_text, wl.dtype), to_dev(wl.k, wl.dtype)
+    lse_dev = torch.from_numpy(lse_o.astype(np.float32)).cuda()
+    s_g, isum_g = A.score_attn(dl, q, k, wl.softmax_scale, row_lse=lse_dev)
+    vis = lay.visual_mask()
+    assert_rel(s_g.cpu().numpy()[vis], s_o[vis], TOL["bf16"], "scores (given lse)")
+    # and the two-pass call agrees bit for bit with a call that is handed its own pass-1 LSE
+    s2, _ = A.score_attn(dl, q, k, wl.softmax_scale)
+    own = A.row_lse(dl, q, k, wl.softmax_scale)
+    s3, _ = A.score_attn(dl, q, k, wl.softmax_scale, row_lse=own)
+    assert torch.equal(s2, s3)
+
+
+@pytest.mark.parametrize("cfg", [4, 5])
+def test_score_parity_sampled_full_size(cfg):
+    """Full-size launch; the oracle computes one sequence's row LSE in full and
+    the scores of sampled visual tokens of that sequence one by one."""
+    wl = workload(cfg, payload=False)
+    lay = wl.layout
+    say(f"[score parity sampled] config {cfg}: B={lay.B} N_tok={lay.N_tok} T={lay.T_tot}")
+    dl = A.DeviceLayout(lay)
+    lse_g, s_g, isum_g, status = gpu_score(wl, dl)
+    assert not status.any()
+    b = lay.B - 1
+    lse_o = O.attn_row_lse(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale, wl.dtype, seqs=[b])
+    t0, t1 = int(lay.cu_text[b]), int(lay.cu_text[b + 1])
+    assert_rel(lse_g[:, t0:t1], lse_o[:, t0:t1], 0.0, "row lse", abs_floor=TOL["bf16"])
+    rng = np.random.default_rng(cfg)
+    s0, s1 = int(lay.cu_seqlens[b]), int(lay.cu_seqlens[b + 1])
+    vis = np.nonzero(lay.visual_mask()[s0:s1])[0] + s0
+    sal = [j for j in vis if wl.salient[j]]
+    sample = np.unique(np.concatenate([rng.choice(vis, 40, replace=False), sal[:8], vis[:2], vis[-2:]]))
+    ref = np.array([O.attn_score_one(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale, wl.dtype,
+                                     lse_o, int(j)) for j in sample])
+    assert_rel(s_g[sample], ref, TOL["bf16"], "sampled scores")
+    # image sums equal the sum of the image's scores (float32, fixed order)
+    for i in range(lay.n_img):
+        st, n = int(lay.img_start[i]), int(lay.img_len[i])
+        assert isum_g[i] == pytest.approx(float(s_g[st:st + n].astype(np.float64).sum()), rel=1e-5)
+    assert np.all(np.isinf(s_g[lay.text_pos]))
+
+
+# ------------------------------------------------------------------ budget
+def _budget_cases():
+    rng = np.random.default_rng(77)
+    cases = []
+    for t in range(40):
+        m = int(rng.integers(1, 33))
+        n = [int(x) for x in rng.integers(1, 1600, size=m)]
+        if t % 7 == 0:
+            n[0] = 0 if m > 1 else n[0]                 # an empty image
+        alpha = [0.0, 1.0, 2.0, 5.0][t % 4]
+        floor_abs = [0, 16, 3][t % 3]
+        mode = O.BUDGET_RAW if t % 5 == 4 else O.BUDGET_PROPORTIONAL
+        S = (rng.lognormal(0.0, 1.0 + (t % 3), size=m) * np.array(n) / 100).astype(np.float32)
+        if t % 11 == 3:
+            S[:] = 0.0                                  # no importance at all
+        if t % 13 == 5:
+            S[int(rng.integers(0, m))] = 0.0
+        cases.append((n, S, alpha, floor_abs, mode))
+    return cases
+
+
+def test_budget_bit_exact_on_same_image_sums():
+    cases = _budget_cases()
+    rng = np.random.default_rng(5)
+    imgs, sums, keeps = [], [], []
+    for n, S, alpha, fa, mode in cases:
+        lo = sum(O.budget_bounds(x, 50, 950, fa)[0] for x in n)
+        hi = sum(O.budget_bounds(x, 50, 950, fa)[1] for x in n)
+        keeps.append(int(rng.integers(lo, hi + 1)) if hi >= lo else None)
+    for (n, S, alpha, fa, mode), K in zip(cases, keeps):
+        if K is None:
+            continue
+        lay = build_layout([n], 1, 2, 0)
+        lay.keep_total[:] = K
+        dl = A.DeviceLayout(lay)
+        say(f"[budget] m={len(n)} K={K} alpha={alpha} floor={fa} mode={mode}")
+        img_sum = torch.from_numpy(S).cuda()
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+        g = A.budget(dl, img_sum, alpha, 50, 950, fa, mode, status=status).cpu().numpy()
+        o = O.budget(lay, S, alpha, 50, 950, fa, mode)
+        assert np.array_equal(g, o), (n, S, alpha, fa, mode, K, g, o)
+        assert not status.any()
+
+
+@pytest.mark.parametrize("K_at", ["lo", "hi"])
+def test_budget_at_bounds(K_at):
+    n = [40, 7, 300, 1]
+    lo = sum(O.budget_bounds(x, 50, 950, 4)[0] for x in n)
+    hi = sum(O.budget_bounds(x, 50, 950, 4)[1] for x in n)
+    lay = build_layout([n], 0, 3, 0)
+    lay.keep_total[:] = lo if K_at == "lo" else hi
+    dl = A.DeviceLayout(lay)
+    S = np.array([5.0, 1.0, 0.5, 9.0], np.float32)
+    g = A.budget(dl, torch.from_numpy(S).cuda(), 1.0, 50, 950, 4).cpu().numpy()
+    assert np.array_equal(g, O.budget(lay, S, 1.0, 50, 950, 4))
+
+
+# ------------------------------------------------------------------ select
+def _sel_layout():
+    return build_layout([[37, 1, 0, 300], [5, 64], [1000]], 3, 5, 40)
+
+
+@pytest.mark.parametrize("pattern", ["random", "ties", "specials"])
+def test_select_bit_exact(pattern):
+    lay = _sel_layout()
+    rng = np.random.default_rng(len(pattern))
+    s = np.full(lay.N_tok, np.inf, np.float32)
+    for i in range(lay.n_img):
+        st, n = int(lay.img_start[i]), int(lay.img_len[i])
+        if pattern == "random":
+            v = rng.standard_normal(n).astype(np.float32)
+        elif pattern == "ties":
+            v = (rng.integers(0, 4, size=n) / 8).astype(np.float32)
+        else:
+            v = rng.choice(np.array([np.nan, -0.0, 0.0, -np.inf, 1e-30, -1e-30, 3.0], np.float32), n)
+        s[st:st + n] = v
+    budgets = np.array([int(rng.integers(0, n + 1)) for n in lay.img_len], np.int32)
+    budgets[0] = lay.img_len[0]                     # keep a whole image
+    dl = A.DeviceLayout({**{nm: getattr(lay, nm) for nm in A.DeviceLayout.NAMES},
+                         "keep_total": [int(budgets[lay.cu_img[b]:lay.cu_img[b + 1]].sum())
+                                        for b in range(lay.B)]})
+    say(f"[select] pattern={pattern}")
+    keep, cu = A.select(dl, torch.from_numpy(s).cuda(), torch.from_numpy(budgets).cuda())
+    keep_o, cu_o = O.select(lay, s, budgets)
+    assert np.array_equal(keep.cpu().numpy(), keep_o)
+    assert np.array_equal(cu.cpu().numpy(), cu_o)
+
+
+# ------------------------------------------------------------------ compact
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_compact_bit_exact(cfg):
+    wl = workload(cfg, payload=True)
+    lay = wl.layout
+    say(f"[compact] config {cfg}")
+    dl = A.DeviceLayout(lay)
+    rng = np.random.default_rng(cfg)
+    # oracle keep list from random scores and oracle budgets
+    s = rng.random(lay.N_tok).astype(np.float32)
+    bud = O.budget(lay, np.array([s[a:a + n].sum() for a, n in zip(lay.img_start, lay.img_len)],
+                                 np.float32), 1.0)
+    keep, _ = O.select(lay, s, bud)
+    keep_d = torch.from_numpy(keep).cuda()
+    hid = to_dev(wl.hidden_states, wl.dtype)
+    pos = torch.from_numpy(wl.pos).cuda()
+    kd, vd = to_dev(wl.k, wl.dtype), to_dev(wl.v, wl.dtype)
+    v_hm = vd.transpose(0, 1).contiguous()          # head-major [Hkv, N, d]
+    outs = A.compact_new(dl, keep_d, [(hid, 0), (pos, 1), (kd, 0), (vd, 0), (v_hm, 1)])
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host_bits(outs[0]), O.compact(keep, wl.hidden_states))
+    assert np.array_equal(outs[1].cpu().numpy(), O.compact(keep, wl.pos, axis=1))
+    assert np.array_equal(to_host_bits(outs[2]), O.compact(keep, wl.k))
+    assert np.array_equal(to_host_bits(outs[3]), O.compact(keep, wl.v))
+    assert np.array_equal(to_host_bits(outs[4]), O.compact(keep, np.swapaxes(wl.v, 0, 1), axis=1))
+
+
+def test_compact_odd_row_sizes():
+    lay = build_layout([[5, 9]], 2, 3, 50)
+    dl = A.DeviceLayout(lay)
+    rng = np.random.default_rng(3)
+    keep = np.sort(rng.choice(lay.N_tok, dl.N_out, replace=False)).astype(np.int32)
+    keep_d = torch.from_numpy(keep).cuda()
+    for shape, dt in [((lay.N_tok, 3), torch.uint8), ((lay.N_tok, 5), torch.int16),
+                      ((lay.N_tok, 7), torch.float32), ((lay.N_tok, 33, 2), torch.bfloat16)]:
+        x = torch.randint(0, 100, shape, dtype=torch.int32).to(dt).cuda()
+        (out,) = A.compact_new(dl, keep_d, [(x, 0)])
+        assert torch.equal(out.cpu(), x.cpu()[torch.from_numpy(keep).long()])
+
+
+# ------------------------------------------------------------------ end to end
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_end_to_end(cfg):
+    wl = workload(cfg, payload=True)
+    lay = wl.layout
+    say(f"[end to end] config {cfg}")
+    dl = A.DeviceLayout(lay)
+    tol = TOL[wl.dtype]
+    q, k = to_dev(wl.q_text, wl.dtype), to_dev(wl.k, wl.dtype)
+    status = torch.zeros(dl.B, dtype=torch.int32, device="cuda")
+    s_g, isum_g = A.score_attn(dl, q, k, wl.softmax_scale, status=status)
+    bud_g = A.budget(dl, isum_g, wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs, status=status)
+    keep_g, cu_g = A.select(dl, s_g, bud_g, status=status)
+    hid = to_dev(wl.hidden_states, wl.dtype)
+    (hid_out,) = A.compact_new(dl, keep_g, [(hid, 0)])
+    torch.cuda.synchronize()
+    assert not status.cpu().numpy().any()
+    s_g, isum_g, bud_g = s_g.cpu().numpy(), isum_g.cpu().numpy(), bud_g.cpu().numpy()
+    keep_g, cu_g = keep_g.cpu().numpy(), cu_g.cpu().numpy()
+
+    s_o, isum_o, _, _ = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale, wl.dtype,
+                                      exact_dot=(cfg == 1))
+    vis = lay.visual_mask()
+    assert_rel(s_g[vis], s_o[vis], tol, "scores")
+    # budgets: bit-exact on the GPU's image sums; the oracle's own sums agree within tol
+    assert np.array_equal(bud_g, O.budget(lay, isum_g, wl.alpha, wl.lo_permille, wl.hi_permille,
+                                          wl.floor_abs))
+    bud_o = O.budget(lay, isum_o.astype(np.float32), wl.alpha, wl.lo_permille, wl.hi_permille,
+                     wl.floor_abs)
+    # selection: bit-exact on the GPU's scores and budgets
+    keep_s, cu_s = O.select(lay, s_g, bud_g)
+    assert np.array_equal(keep_g, keep_s) and np.array_equal(cu_g, cu_s)
+    # against the oracle chain: identical outside the threshold band (images with equal budgets)
+    keep_o, _ = O.select(lay, s_o.astype(np.float32), bud_o)
+    same = bud_g == bud_o
+    for i in np.nonzero(same)[0]:
+        st, n = int(lay.img_start[i]), int(lay.img_len[i])
+        gi = [x for x in keep_g if st <= x < st + n]
+        oi = [x for x in keep_o if st <= x < st + n]
+        kept_sets_match(lay, gi, oi, s_o, bud_o, tol)
+    # compaction bit-exact given the indices; text always kept; order preserved
+    assert np.array_equal(to_host_bits(hid_out), O.compact(keep_g, wl.hidden_states))
+    assert set(lay.text_pos.tolist()) <= set(keep_g.tolist())
+    for b in range(lay.B):
+        seg = keep_g[cu_g[b]:cu_g[b + 1]]
+        assert np.all(np.diff(seg) > 0)
+        assert len(seg) == (lay.cu_text[b + 1] - lay.cu_text[b]) + lay.keep_total[b]
+
+
+def test_config1_exact_ties_keep_lowest_index():
+    wl = make_workload(1, payload=False)
+    lay = wl.layout
+    s_o, isum_o, _, _ = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale, "fp32",
+                                      exact_dot=True)
+    bud = O.budget(lay, isum_o.astype(np.float32), 1.0)
+    st, n = int(lay.img_start[1]), int(lay.img_len[1])
+    k1 = int(bud[1])
+    order = sorted(range(st, st + n), key=lambda j: (-s_o[j], j))
+    group = order[k1 - 2:k1 + 2]
+    src = min(group, key=lambda j: (-s_o[j], j))       # the highest-ranked member
+    duplicate_key_rows(wl, src, [j for j in group if j != src])
+    s_o, isum_o, _, _ = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale, "fp32",
+                                      exact_dot=True)
+    assert len({s_o[j] for j in group}) == 1            # four exact ties in the oracle
+    dl = A.DeviceLayout(lay)
+    q, k = to_dev(wl.q_text, "fp32"), to_dev(wl.k, "fp32")
+    s_g, isum_g = A.score_attn(dl, q, k, wl.softmax_scale)
+    s_gn = s_g.cpu().numpy()
+    assert len({float(s_gn[j]) for j in group}) == 1    # and bit-identical on the GPU
+    bud_g = A.budget(dl, isum_g, 1.0)
+    keep_g, _ = A.select(dl, s_g, bud_g)
+    keep_g = set(keep_g.cpu().numpy().tolist())
+    kept = sorted(j for j in group if j in keep_g)
+    assert 0 < len(kept) < 4
+    assert kept == sorted(group)[:len(kept)]           # the lowest indices win the tie
+    bud_o = O.budget(lay, isum_o.astype(np.float32), 1.0)
+    keep_o, _ = O.select(lay, s_o.astype(np.float32), bud_o)
+    if np.array_equal(bud_g.cpu().numpy(), bud_o):
+        assert keep_g == set(keep_o.tolist())
+
+
+# ------------------------------------------------------------------ variation mode
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_variation_parity(cfg):
+    wl = workload(cfg, payload=False, variation=True)
+    lay = wl.layout
+    say(f"[variation] config {cfg}")
+    dl = A.DeviceLayout(lay)
+    hc, hp = to_dev(wl.h_cur, wl.dtype), to_dev(wl.h_prior, wl.dtype)
+    s_g, isum_g = A.score_variation(dl, hc, hp)
+    s_o, isum_o = O.variation_scores(lay, wl.h_cur, wl.h_prior, wl.dtype)
+    vis = lay.visual_mask()
+    assert_rel(s_g.cpu().numpy()[vis], s_o[vis], TOL[wl.dtype], "variation scores", abs_floor=1e-6)
+    assert_rel(isum_g.cpu().numpy(), isum_o, TOL[wl.dtype], "variation sums", abs_floor=1e-5)
+    assert np.all(np.isinf(s_g.cpu().numpy()[~vis]))
+
+
+# ------------------------------------------------------------------ edge layouts
+def test_edge_layout_ragged_empty_and_no_text_after():
+    """Empty image, single-token image, ragged lengths, a sequence without
+    images, and an image with no text row after it (flagged, scores 0)."""
+    lay = build_layout([[0, 1, 33, 70], [], [65]], 2, 3, 50)
+    # drop the tail text of the last sequence so its image has no text after it
+    # (rebuild by hand: text, image of 65, nothing after)
+    arrays = {n: np.array(getattr(lay, n)) for n in A.DeviceLayout.NAMES}
+    b = 2
+    s0 = int(lay.cu_seqlens[b])
+    t0 = int(lay.cu_text[b])
+    arrays["text_pos"] = np.concatenate([lay.text_pos[:t0], np.arange(s0, s0 + 2)]).astype(np.int32)
+    arrays["cu_text"] = np.array([0, lay.cu_text[1], lay.cu_text[2], lay.cu_text[2] + 2], np.int32)
+    arrays["cu_seqlens"] = np.array([0, lay.cu_seqlens[1], lay.cu_seqlens[2], s0 + 2 + 65], np.int32)
+    arrays["keep_total"] = np.array([lay.keep_total[0], 0, 33], np.int32)
+    lay2 = Layout(**arrays)
+    dl = A.DeviceLayout(lay2)
+    rng = np.random.default_rng(1)
+    Hq, Hkv, d = 8, 2, 128
+    q32 = rng.standard_normal((lay2.T_tot, Hq, d)).astype(np.float32)
+    k32 = rng.standard_normal((lay2.N_tok, Hkv, d)).astype(np.float32)
+    qb, kb = f32_to_bf16_bits(q32), f32_to_bf16_bits(k32)
+    status = torch.zeros(3, dtype=torch.int32, device="cuda")
+    s_g, isum_g = A.score_attn(dl, to_dev(qb, "bf16"), to_dev(kb, "bf16"), d ** -0.5, status=status)
+    s_o, isum_o, _, empty = O.attn_scores(lay2, qb, kb, Hq, Hkv, d ** -0.5, "bf16")
+    vis = lay2.visual_mask()
+    s_gn = s_g.cpu().numpy()
+    assert_rel(s_gn[vis], s_o[vis], TOL["bf16"], "scores", abs_floor=1e-30)
+    assert_rel(isum_g.cpu().numpy(), isum_o, TOL["bf16"], "sums", abs_floor=1e-30)
+    st = status.cpu().numpy()
+    assert st[2] & A.FLAG_NO_TEXT_AFTER and not st[0] and not st[1]
+    assert empty == {lay2.n_img - 1}
+    bud_g = A.budget(dl, isum_g, 1.0)
+    keep_g, cu_g = A.select(dl, s_g, bud_g)
+    keep_s, cu_s = O.select(lay2, s_gn, bud_g.cpu().numpy())
+    assert np.array_equal(keep_g.cpu().numpy(), keep_s) and np.array_equal(cu_g.cpu().numpy(), cu_s)
