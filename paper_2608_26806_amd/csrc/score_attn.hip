@@ -76,7 +76,43 @@ struct Geo {
   static constexpr int NT2 = tiles_pass2(ROWB);   // same for pass 2
   static constexpr int V16 = kStage * ROWB / 16 / kThreads;  // 16-byte loads per thread per stage
   static constexpr int V16_ROW = ROWB / 16;
+  static constexpr int NCH = ROWB / 16;                // 16-byte chunks per row
+  static constexpr int SWZ = (NCH < 16 ? NCH : 16) - 1;  // XOR swizzle of the chunk index
+  static constexpr int DMA = kStage * NCH / 64 / 4;    // direct-to-LDS loads per wave per stage
+  static_assert(DMA >= 1 && kStage * NCH % 256 == 0, "stage must split into whole wave loads");
 };
+
+// Byte offset in a swizzled LDS stage of element offset `eo` of row `row`:
+// row-major rows without padding, the 16-byte chunk index XOR-ed with the
+// row so that the 32 rows read by one MFMA operand load hit distinct banks.
+template <typename T, int D>
+__device__ inline int swz_off(int row, int eo) {
+  using G_ = Geo<T, D>;
+  const int bo = eo * (int)sizeof(T);
+  return row * G_::ROWB + (((bo >> 4) ^ (row & G_::SWZ)) << 4) + (bo & 15);
+}
+
+// Enqueue one stage (kStage rows of ROWB bytes) with global_load_lds: wave w
+// fills LDS bytes [1 KB * (w*DMA + i), +1 KB) for i < DMA, lane l writing
+// the 16 bytes at +16*l, i.e. physical chunk p = 64*(w*DMA+i) + l.
+// row_src(row) returns the global address of a row (always a valid row).
+template <typename T, int D, typename F>
+__device__ inline void dma_stage(char *lds, int wave, int lane, F row_src) {
+  using G_ = Geo<T, D>;
+#pragma unroll
+  for (int i = 0; i < G_::DMA; ++i) {
+    const int gi = wave * G_::DMA + i;
+    const int p = gi * 64 + lane;
+    const int row = p / G_::NCH, pc = p % G_::NCH;
+    const int c = pc ^ (row & G_::SWZ);
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void *)(row_src(row) + c * 16),
+        (__attribute__((address_space(3))) void *)(lds + gi * 1024), 16, 0, 0);
+  }
+}
+
+// wait for this wave's outstanding global loads (including direct-to-LDS ones)
+__device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0xF70); }
 
 template <typename F>
 __device__ inline F load_frag(const char *p) {
@@ -107,6 +143,13 @@ struct P1Args {
 
 // Pass 1: per (sequence b, key head g, query block, key chunk), partial
 // row statistics (max in log2 units, sum of 2^(z - max)) of every query row.
+//
+// Per 32-key tile a wave runs NT chains of 8 MFMAs (one per stationary
+// query tile).  The exp/sum of chain i-1 is issued in the same basic block
+// as the MFMAs of chain i, so the transcendental work runs while the matrix
+// core is busy.  The running maximum is only raised when a tile's sum of
+// 2^(z - m) exceeds 2^64 (first visible tile, or a big jump): the common
+// case costs one FMA, one exp and one add per logit.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
   using G_ = Geo<T, D>;
@@ -114,7 +157,7 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
   using frag = typename MM::frag;
   constexpr int NT = G_::NT1, NS = G_::NS, ROWB = G_::ROWB, LS = G_::LS, E = G_::E;
   constexpr int QB = 4 * NT * 32;  // query rows per block
-  __shared__ __attribute__((aligned(16))) char smem[kStage * LS];
+  __shared__ __attribute__((aligned(16))) char smem[2][kStage * LS];
 
   // Blocks that share one key chunk (the nqb query blocks of a unit) get
   // ids that are equal mod 8, i.e. land on one XCD and share its L2.
@@ -147,17 +190,14 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
 
   // stationary operand: this wave's query rows
   frag qf[NT][NS];
-  int qpos[NT];
-  int qidx[NT];
+  int qrel[NT];  // query position relative to the sequence start (-1: padding row)
 #pragma unroll
   for (int i = 0; i < NT; ++i) {
     const int r = wr0 + i * 32 + col;
-    qpos[i] = -1;
-    qidx[i] = -1;
+    qrel[i] = -1;
     if (r < R) {
       const int hh = r / Tb, t = r - hh * Tb, h = g * a.G + hh;
-      qpos[i] = tp[t];
-      qidx[i] = h * a.T_tot + t0 + t;
+      qrel[i] = tp[t] - s0;
       const char *src = a.q + ((size_t)(t0 + t) * a.Hq + h) * ROWB + hi * E * sizeof(T);
 #pragma unroll
       for (int s = 0; s < NS; ++s) qf[i][s] = load_frag<frag>(src + s * 2 * E * sizeof(T));
@@ -173,99 +213,121 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
     m2[i] = -INFINITY;
     l[i] = 0.f;
   }
+  const float cl2e = a.cl2e;
 
-  // cooperative stage loader: kStage key rows of head g -> registers -> LDS
-  uint4 pre[G_::V16];
-  auto load_stage = [&](int ks) {
-#pragma unroll
-    for (int v = 0; v < G_::V16; ++v) {
-      const int idx = tid + v * kThreads;
-      const int row = idx / G_::V16_ROW, c16 = idx % G_::V16_ROW;
-      const int key = ks + row;
-      if (key < kend)
-        pre[v] = *reinterpret_cast<const uint4 *>(
-            a.k + ((size_t)(s0 + key) * a.Hkv + g) * ROWB + c16 * 16);
-      else
-        pre[v] = uint4{0, 0, 0, 0};
-    }
+  // keys of one stage, rows clamped into the chunk (rows past kend are masked)
+  auto issue_stage = [&](int ks, int bufi) {
+    dma_stage<T, D>(smem[bufi], wave, lane, [&](int row) {
+      const int key = min(ks + row, kend - 1);
+      return a.k + ((size_t)(s0 + key) * a.Hkv + g) * ROWB;
+    });
   };
-  auto store_stage = [&]() {
+
+  // Accumulator element e of this lane holds key kb + hi*4 + eoff(e) of its
+  // query column; it is visible iff eoff(e) <= vlim, with the per-lane limit
+  // vlim = min(q - kb, kend - 1 - kb) - hi*4 (causal row and chunk end).
+  auto eoff = [](int e) { return 8 * (e >> 2) + (e & 3); };
+  auto vlimit = [&](int qi, int kb) { return min(qrel[qi] - kb, kend - 1 - kb) - hi * 4; };
+
+  // Exact update of row qi with tile kb (any visibility pattern; raises the max).
+  auto exact_update = [&](const f32x16 &acc, int qi, int kb) {
+    const int vl = vlimit(qi, kb);
+    float tm = -INFINITY;
 #pragma unroll
-    for (int v = 0; v < G_::V16; ++v) {
-      const int idx = tid + v * kThreads;
-      const int row = idx / G_::V16_ROW, c16 = idx % G_::V16_ROW;
-      *reinterpret_cast<uint4 *>(smem + row * LS + c16 * 16) = pre[v];
+    for (int e = 0; e < 16; ++e)
+      if (eoff(e) <= vl) tm = fmaxf(tm, acc[e] * cl2e);
+    if (tm == -INFINITY) return;
+    const float nm = fmaxf(m2[qi], tm);
+    float ns = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float x = __builtin_amdgcn_exp2f(acc[e] * cl2e - nm);
+      ns += eoff(e) <= vl ? x : 0.f;
     }
+    l[qi] = l[qi] * __builtin_amdgcn_exp2f(m2[qi] - nm) + ns;
+    m2[qi] = nm;
   };
+
+  f32x16 pacc = f32x16{};  // accumulators waiting for their exp/sum
+  int pend_kb = 0;
+  bool pend = false;
 
   const int nstage = (kstop - kbeg + kStage - 1) / kStage;
-  load_stage(kbeg);
+  issue_stage(kbeg, 0);
   for (int st = 0; st < nstage; ++st) {
     const int ks = kbeg + st * kStage;
-    __syncthreads();
-    store_stage();
-    __syncthreads();
-    if (st + 1 < nstage) load_stage(ks + kStage);
-    if (!active) continue;
+    wait_vmem();
+    __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
+    if (st + 1 < nstage) issue_stage(ks + kStage, (st + 1) & 1);
+    const char *buf = smem[st & 1];
+    if (active) {
 #pragma unroll
-    for (int kt = 0; kt < kStage / 32; ++kt) {
-      const int kb = ks + kt * 32;  // first key (relative) of this 32-key tile
-      if (kb >= kstop || s0 + kb > wmax) break;  // later tiles are invisible too
-      const bool masked = (kb + 32 > kend) || (s0 + kb + 31 > wmin);
-      f32x16 acc[NT];
+      for (int kt = 0; kt < kStage / 32; ++kt) {
+        const int kb = ks + kt * 32;  // first key (relative) of this 32-key tile
+        if (kb < kstop && s0 + kb <= wmax) {
+          frag av[NS];
 #pragma unroll
-      for (int i = 0; i < NT; ++i) acc[i] = f32x16{};
-      const char *arow = smem + (kt * 32 + col) * LS + hi * E * sizeof(T);
+          for (int s = 0; s < NS; ++s)
+            av[s] = load_frag<frag>(buf + swz_off<T, D>(kt * 32 + col, s * 2 * E + hi * E));
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const frag av = load_frag<frag>(arow + s * 2 * E * sizeof(T));
+          for (int qi = 0; qi < NT; ++qi) {
+            const int pqi = qi == 0 ? NT - 1 : qi - 1;
+            const int pkb = qi == 0 ? pend_kb : kb;
+            const bool has = qi > 0 || pend;
+            // visibility of the pending tile for this lane: all, none, or partial
+            const int vl = vlimit(pqi, pkb);
+            const bool none = qrel[pqi] - pkb < 0;
+            const bool all = qrel[pqi] - pkb >= 31 && pkb + 32 <= kend;
+            const bool fast = __ballot(!(none || all)) == 0ull;
+            f32x16 acc = f32x16{};
+            float ts = 0.f;
+            if (has && fast) {
 #pragma unroll
-        for (int i = 0; i < NT; ++i) acc[i] = MM::run(av, qf[i][s], acc[i]);
-      }
-      // lane holds keys kb + hi*4 + 8*(e/4) + e%4, e = 0..15, of query column `col`
+              for (int s = 0; s < NS; ++s) {
+                acc = MM::run(av[s], qf[qi][s], acc);
 #pragma unroll
-      for (int i = 0; i < NT; ++i) {
-        float ts = 0.f;
-        if (!masked) {
+                for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e)
+                  ts += __builtin_amdgcn_exp2f(pacc[e] * cl2e - m2[pqi]);
+              }
+              if (none) ts = 0.f;
+            } else if (has) {
 #pragma unroll
-          for (int e = 0; e < 16; ++e) ts += __builtin_amdgcn_exp2f(acc[i][e] * a.cl2e - m2[i]);
-        } else {
+              for (int s = 0; s < NS; ++s) {
+                acc = MM::run(av[s], qf[qi][s], acc);
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = kb + hi * 4 + 8 * (e >> 2) + (e & 3);
-            const bool vis = key < kend && s0 + key <= qpos[i];
-            const float x = __builtin_amdgcn_exp2f(acc[i][e] * a.cl2e - m2[i]);
-            ts += vis ? x : 0.f;
+                for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e) {
+                  const float x = __builtin_amdgcn_exp2f(pacc[e] * cl2e - m2[pqi]);
+                  ts += eoff(e) <= vl ? x : 0.f;
+                }
+              }
+            } else {
+#pragma unroll
+              for (int s = 0; s < NS; ++s) acc = MM::run(av[s], qf[qi][s], acc);
+            }
+            if (has) {
+              if (ts <= 0x1p64f) l[pqi] += ts;
+              else exact_update(pacc, pqi, pkb);  // first visible tile, a jump, or NaN
+            }
+            pacc = acc;
           }
+          pend = true;
+          pend_kb = kb;
         }
-        if (ts <= 0x1p64f) {  // common case: no new maximum worth rescaling for
-          l[i] += ts;
-          continue;
-        }
-        // first visible tile of this row, a jump of the maximum, or NaN
-        float tm = -INFINITY;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = kb + hi * 4 + 8 * (e >> 2) + (e & 3);
-          const bool vis = !masked || (key < kend && s0 + key <= qpos[i]);
-          if (vis) tm = fmaxf(tm, acc[i][e] * a.cl2e);
-        }
-        if (tm == -INFINITY) continue;
-        const float nm = fmaxf(m2[i], tm);
-        float ns = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = kb + hi * 4 + 8 * (e >> 2) + (e & 3);
-          const bool vis = !masked || (key < kend && s0 + key <= qpos[i]);
-          const float x = __builtin_amdgcn_exp2f(acc[i][e] * a.cl2e - nm);
-          ns += vis ? x : 0.f;
-        }
-        l[i] = l[i] * __builtin_amdgcn_exp2f(m2[i] - nm) + ns;
-        m2[i] = nm;
       }
     }
   }
   if (!active) return;
+  if (pend) {
+    const int vl = vlimit(NT - 1, pend_kb);
+    float ts = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float x = __builtin_amdgcn_exp2f(pacc[e] * cl2e - m2[NT - 1]);
+      ts += eoff(e) <= vl ? x : 0.f;
+    }
+    if (ts <= 0x1p64f) l[NT - 1] += ts;
+    else exact_update(pacc, NT - 1, pend_kb);
+  }
   // merge the two half-waves (same query column, disjoint keys) and store
   const size_t HqT = (size_t)a.Hq * a.T_tot;
 #pragma unroll
@@ -275,9 +337,11 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
     float tot = 0.f;
     if (nm != -INFINITY)
       tot = l[i] * __builtin_amdgcn_exp2f(m2[i] - nm) + ol * __builtin_amdgcn_exp2f(om - nm);
-    if (hi == 0 && qidx[i] >= 0) {
-      a.part_m[kc * HqT + qidx[i]] = nm;
-      a.part_l[kc * HqT + qidx[i]] = tot;
+    const int r = wr0 + i * 32 + col;
+    if (hi == 0 && r < R) {
+      const int hh = r / Tb, qidx = (g * a.G + hh) * a.T_tot + t0 + (r - hh * Tb);
+      a.part_m[kc * HqT + qidx] = nm;
+      a.part_l[kc * HqT + qidx] = tot;
     }
   }
 }
@@ -321,16 +385,23 @@ struct P2Args {
 
 // Pass 2: per (sequence b, key head g, key block), the column sums
 // sum_{h in group g} sum_t exp(c q_{t,h}.k_j - lse[h,t]) over visible rows.
+//
+// Query tiles (and their LSE, positions and position range) stream through
+// double-buffered LDS; keys are the stationary MFMA operand.  For a 32-row
+// tile that sees every key of the wave, the exp/sum of key tile j-1 is
+// issued between the MFMAs of key tile j; tiles that see only part of the
+// wave's keys take a masked path, tiles that see none are skipped.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   using G_ = Geo<T, D>;
   using MM = Mma<T>;
   using frag = typename MM::frag;
-  constexpr int NKT = G_::NT2, NS = G_::NS, ROWB = G_::ROWB, LS = G_::LS, E = G_::E;
+  constexpr int NKT = G_::NT2, NS = G_::NS, ROWB = G_::ROWB, E = G_::E;
   constexpr int KB = 4 * NKT * 32;  // keys per block
-  __shared__ __attribute__((aligned(16))) char smem[kStage * LS];
-  __shared__ __attribute__((aligned(16))) float s_lse2[kStage];
-  __shared__ int s_pos[kStage];
+  __shared__ __attribute__((aligned(16))) char smem[2][kStage * ROWB];
+  __shared__ __attribute__((aligned(16))) float s_lse2[2][kStage];
+  __shared__ __attribute__((aligned(16))) int s_pos[2][kStage];
+  __shared__ int s_meta[2][4];  // per 32-row half: min and max position
 
   // the nkb key blocks of one (sequence, key head) read the same queries:
   // keep them on one XCD
@@ -372,103 +443,154 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   float cs[NKT];
 #pragma unroll
   for (int j = 0; j < NKT; ++j) cs[j] = 0.f;
+  const float cl2e = a.cl2e;
 
-  uint4 pre[G_::V16];
-  float pre_lse = 0.f;
+  auto issue_stage = [&](int rs, int bufi) {
+    dma_stage<T, D>(smem[bufi], wave, lane, [&](int row) {
+      const int r = min(rs + row, R - 1);  // padding rows re-read row R-1; their lse is +inf
+      const int hh = r / Tb, t = r - hh * Tb;
+      return a.q + ((size_t)(t0 + t) * a.Hq + g * a.G + hh) * ROWB;
+    });
+  };
+  float pre_lse = INFINITY;
   int pre_pos = -1;
-  auto load_stage = [&](int rs) {
-#pragma unroll
-    for (int v = 0; v < G_::V16; ++v) {
-      const int idx = tid + v * kThreads;
-      const int row = idx / G_::V16_ROW, c16 = idx % G_::V16_ROW;
-      const int r = rs + row;
-      if (r < R) {
-        const int hh = r / Tb, t = r - hh * Tb;
-        pre[v] = *reinterpret_cast<const uint4 *>(
-            a.q + ((size_t)(t0 + t) * a.Hq + g * a.G + hh) * ROWB + c16 * 16);
-      } else {
-        pre[v] = uint4{0, 0, 0, 0};
-      }
-    }
-    if (tid < kStage) {
-      const int r = rs + tid;
+  auto load_meta = [&](int rs) {  // wave 0: LSE (log2 units) and position of each row
+    if (wave == 0) {
+      const int r = rs + lane;
+      pre_lse = INFINITY;
+      pre_pos = -1;
       if (r < R) {
         const int hh = r / Tb, t = r - hh * Tb;
         pre_lse = a.lse[(size_t)(g * a.G + hh) * a.T_tot + t0 + t] * kLog2e;
         pre_pos = tp[t];
-      } else {
-        pre_lse = INFINITY;  // padding rows contribute exp2(-inf) = 0
-        pre_pos = -1;
       }
     }
   };
-  auto store_stage = [&]() {
+  auto store_meta = [&](int bufi) {
+    if (wave == 0) {
+      s_lse2[bufi][lane] = pre_lse;
+      s_pos[bufi][lane] = pre_pos;
+      int vmin = pre_pos >= 0 ? pre_pos : 0x7fffffff, vmax = pre_pos;
 #pragma unroll
-    for (int v = 0; v < G_::V16; ++v) {
-      const int idx = tid + v * kThreads;
-      const int row = idx / G_::V16_ROW, c16 = idx % G_::V16_ROW;
-      *reinterpret_cast<uint4 *>(smem + row * LS + c16 * 16) = pre[v];
-    }
-    if (tid < kStage) {
-      s_lse2[tid] = pre_lse;
-      s_pos[tid] = pre_pos;
+      for (int off = 16; off > 0; off >>= 1) {  // reduce within each 32-lane half
+        vmin = min(vmin, __shfl_xor(vmin, off));
+        vmax = max(vmax, __shfl_xor(vmax, off));
+      }
+      if (col == 0) {
+        s_meta[bufi][2 * hi] = vmin;
+        s_meta[bufi][2 * hi + 1] = vmax;
+      }
     }
   };
 
+  auto exp_sum = [&](const f32x16 &acc, const float *lv) {
+    float t = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) t += __builtin_amdgcn_exp2f(acc[e] * cl2e - lv[e]);
+    return t;
+  };
+
+  f32x16 pacc = f32x16{};
+  float plv[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) plv[e] = INFINITY;
+  bool pend = false;  // pacc holds key tile NKT-1 of an earlier row tile
+
   const int nstage = (R + kStage - 1) / kStage;
-  if (nstage > 0) load_stage(0);
+  if (nstage > 0) {
+    issue_stage(0, 0);
+    load_meta(0);
+    store_meta(0);
+  }
   for (int st = 0; st < nstage; ++st) {
     const int rs = st * kStage;
-    __syncthreads();
-    store_stage();
-    __syncthreads();
-    if (st + 1 < nstage) load_stage(rs + kStage);
-    if (!active) continue;
+    const int bi = st & 1;
+    wait_vmem();
+    __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
+    if (st + 1 < nstage) {
+      issue_stage(rs + kStage, bi ^ 1);
+      load_meta(rs + kStage);
+    }
+    if (active) {
 #pragma unroll
-    for (int sub = 0; sub < kStage / 32; ++sub) {
-      const int r0 = rs + sub * 32;
-      if (r0 >= R) break;
-      int qmin, qmax;
-      rows_pos_range(tp, Tb, r0, min(R, r0 + 32), qmin, qmax);
-      if (qmax < kmin) continue;  // no row of this tile sees any key of the wave
-      // lane's rows: sub*32 + hi*4 + 8*(e/4) + e%4
-      float lv[16];
+      for (int sub = 0; sub < kStage / 32; ++sub) {
+        if (rs + sub * 32 >= R) break;
+        const int qmin = s_meta[bi][2 * sub], qmax = s_meta[bi][2 * sub + 1];
+        if (qmax < kmin) continue;  // no row of this tile sees any key of the wave
+        frag av[NS];
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const float4 v = *reinterpret_cast<const float4 *>(&s_lse2[sub * 32 + hi * 4 + 8 * e4]);
-        lv[4 * e4 + 0] = v.x;
-        lv[4 * e4 + 1] = v.y;
-        lv[4 * e4 + 2] = v.z;
-        lv[4 * e4 + 3] = v.w;
-      }
-      f32x16 acc[NKT];
+        for (int s = 0; s < NS; ++s)
+          av[s] = load_frag<frag>(smem[bi] + swz_off<T, D>(sub * 32 + col, s * 2 * E + hi * E));
+        // lane's rows: sub*32 + hi*4 + 8*(e/4) + e%4
+        float lv[16];
 #pragma unroll
-      for (int j = 0; j < NKT; ++j) acc[j] = f32x16{};
-      const char *arow = smem + (sub * 32 + col) * LS + hi * E * sizeof(T);
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const float4 v = *reinterpret_cast<const float4 *>(&s_lse2[bi][sub * 32 + hi * 4 + 8 * e4]);
+          lv[4 * e4 + 0] = v.x;
+          lv[4 * e4 + 1] = v.y;
+          lv[4 * e4 + 2] = v.z;
+          lv[4 * e4 + 3] = v.w;
+        }
+        if (qmin >= kmax) {
+          // every row sees every key of the wave: pipelined MFMA + exp/sum
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const frag av = load_frag<frag>(arow + s * 2 * E * sizeof(T));
+          for (int j = 0; j < NKT; ++j) {
+            f32x16 acc = f32x16{};
+            float ts = 0.f;
+            if (j > 0 || pend) {
+              const float *pl = j > 0 ? lv : plv;
 #pragma unroll
-        for (int j = 0; j < NKT; ++j) acc[j] = MM::run(av, kf[j][s], acc[j]);
-      }
+              for (int s = 0; s < NS; ++s) {
+                acc = MM::run(av[s], kf[j][s], acc);
 #pragma unroll
-      for (int j = 0; j < NKT; ++j) {
-        const int tmin = kmin + j * 32, tmaxp = min(kmax, tmin + 31);
-        if (qmin >= tmaxp) {  // every row sees every key of the tile
+                for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e)
+                  ts += __builtin_amdgcn_exp2f(pacc[e] * cl2e - pl[e]);
+              }
+              cs[j > 0 ? j - 1 : NKT - 1] += ts;
+            } else {
 #pragma unroll
-          for (int e = 0; e < 16; ++e) cs[j] += __builtin_amdgcn_exp2f(acc[j][e] * a.cl2e - lv[e]);
-        } else if (qmax >= tmin) {
+              for (int s = 0; s < NS; ++s) acc = MM::run(av[s], kf[j][s], acc);
+            }
+            pacc = acc;
+          }
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int qp = s_pos[sub * 32 + hi * 4 + 8 * (e >> 2) + (e & 3)];
-            const float x = __builtin_amdgcn_exp2f(acc[j][e] * a.cl2e - lv[e]);
-            cs[j] += kpos[j] <= qp ? x : 0.f;
+          for (int e = 0; e < 16; ++e) plv[e] = lv[e];
+          pend = true;
+        } else {
+          // some rows see only part of the wave's keys: masked, not pipelined
+          if (pend) {
+            cs[NKT - 1] += exp_sum(pacc, plv);
+            pend = false;
+          }
+          int qp[16];
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4) {
+            const int4 v = *reinterpret_cast<const int4 *>(&s_pos[bi][sub * 32 + hi * 4 + 8 * e4]);
+            qp[4 * e4 + 0] = v.x;
+            qp[4 * e4 + 1] = v.y;
+            qp[4 * e4 + 2] = v.z;
+            qp[4 * e4 + 3] = v.w;
+          }
+#pragma unroll
+          for (int j = 0; j < NKT; ++j) {
+            f32x16 acc = f32x16{};
+#pragma unroll
+            for (int s = 0; s < NS; ++s) acc = MM::run(av[s], kf[j][s], acc);
+            float ts = 0.f;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const float x = __builtin_amdgcn_exp2f(acc[e] * cl2e - lv[e]);
+              ts += kpos[j] <= qp[e] ? x : 0.f;
+            }
+            cs[j] += ts;
           }
         }
       }
     }
+    if (st + 1 < nstage) store_meta(bi ^ 1);
   }
   if (!active) return;
+  if (pend) cs[NKT - 1] += exp_sum(pacc, plv);
 #pragma unroll
   for (int j = 0; j < NKT; ++j) {
     const float v = cs[j] + __shfl_xor(cs[j], 32);
