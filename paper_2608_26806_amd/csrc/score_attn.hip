@@ -25,6 +25,8 @@
 
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "avtp_internal.h"
 
 namespace avtp {
@@ -35,7 +37,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kThreads = 256;  // 4 waves per block in both passes
-constexpr int kStage = 64;     // rows (keys or queries) per LDS stage
+constexpr int kStage = 64;     // query rows per LDS stage in pass 2
+constexpr int kStage1 = 128;   // key rows per LDS stage in pass 1
 
 template <typename T>
 struct Mma;
@@ -56,15 +59,15 @@ struct Mma<float> {
   }
 };
 
-// Register budget (two waves per SIMD = 256 VGPRs per wave): the stationary
-// operand of a wave, NT tiles of 32 rows, takes at most 128 VGPRs in pass 1
-// (queries; accumulators 16 per tile) and at most 96 in pass 2 (keys; the
-// per-row LSE values of the streamed tile need registers too).
-__host__ __device__ constexpr int tiles_cap(int budget, int row_bytes) {
-  return (budget / (row_bytes / 8)) > 4 ? 4 : (budget / (row_bytes / 8));
+// Register budget, two waves per SIMD (256 VGPRs per wave).  Pass 1: the
+// stationary queries take at most 128 (4 tiles of 32 rows), leaving room for
+// the key fragments and two 16-register accumulator sets.  Pass 2: the
+// stationary keys take at most 96, leaving room for the streamed tile's LSE.
+__host__ __device__ constexpr int tiles_cap(int budget, int row_bytes, int cap) {
+  return (budget / (row_bytes / 8)) > cap ? cap : (budget / (row_bytes / 8));
 }
-__host__ __device__ constexpr int tiles_pass1(int row_bytes) { return tiles_cap(128, row_bytes); }
-__host__ __device__ constexpr int tiles_pass2(int row_bytes) { return tiles_cap(96, row_bytes); }
+__host__ __device__ constexpr int tiles_pass1(int row_bytes) { return tiles_cap(128, row_bytes, 4); }
+__host__ __device__ constexpr int tiles_pass2(int row_bytes) { return tiles_cap(96, row_bytes, 4); }
 
 template <typename T, int D>
 struct Geo {
@@ -78,8 +81,6 @@ struct Geo {
   static constexpr int V16_ROW = ROWB / 16;
   static constexpr int NCH = ROWB / 16;                // 16-byte chunks per row
   static constexpr int SWZ = (NCH < 16 ? NCH : 16) - 1;  // XOR swizzle of the chunk index
-  static constexpr int DMA = kStage * NCH / 64 / 4;    // direct-to-LDS loads per wave per stage
-  static_assert(DMA >= 1 && kStage * NCH % 256 == 0, "stage must split into whole wave loads");
 };
 
 // Byte offset in a swizzled LDS stage of element offset `eo` of row `row`:
@@ -92,22 +93,42 @@ __device__ inline int swz_off(int row, int eo) {
   return row * G_::ROWB + (((bo >> 4) ^ (row & G_::SWZ)) << 4) + (bo & 15);
 }
 
-// Enqueue one stage (kStage rows of ROWB bytes) with global_load_lds: wave w
+// Enqueue one stage (ROWS rows of ROWB bytes) with global_load_lds: wave w
 // fills LDS bytes [1 KB * (w*DMA + i), +1 KB) for i < DMA, lane l writing
 // the 16 bytes at +16*l, i.e. physical chunk p = 64*(w*DMA+i) + l.
-// row_src(row) returns the global address of a row (always a valid row).
-template <typename T, int D, typename F>
-__device__ inline void dma_stage(char *lds, int wave, int lane, F row_src) {
+// row_off(row) is the byte offset of a (valid) source row from the
+// wave-uniform `base`.  The lane id is made opaque so that the few integer
+// ops per load are redone per stage instead of pinning registers.
+template <typename T, int D, int ROWS, typename F>
+__device__ inline void dma_stage(char *lds, const char *base, int wave, int lane, F row_off) {
   using G_ = Geo<T, D>;
+  constexpr int DMA = ROWS * G_::NCH / 64 / 4;  // 1 KB loads per wave
+  static_assert(DMA >= 1 && ROWS * G_::NCH % 256 == 0, "stage must split into whole wave loads");
+  int ln = lane;
+  asm volatile("" : "+v"(ln));
 #pragma unroll
-  for (int i = 0; i < G_::DMA; ++i) {
-    const int gi = wave * G_::DMA + i;
-    const int p = gi * 64 + lane;
-    const int row = p / G_::NCH, pc = p % G_::NCH;
+  for (int i = 0; i < DMA; ++i) {
+    const int gi = wave * DMA + i;
+    const unsigned p = (unsigned)(gi * 64 + ln);
+    const int row = (int)(p / G_::NCH), pc = (int)(p % G_::NCH);
     const int c = pc ^ (row & G_::SWZ);
-    __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void *)(row_src(row) + c * 16),
-        (__attribute__((address_space(3))) void *)(lds + gi * 1024), 16, 0, 0);
+    const uint32_t off = row_off(row) + (uint32_t)(c * 16);
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(base + off),
+                                     (__attribute__((address_space(3))) void *)(lds + gi * 1024),
+                                     16, 0, 0);
+  }
+}
+
+// Scheduling hint for one MFMA chain of NS steps sharing a basic block with
+// independent VALU work: issue one MFMA, then up to V VALU ops, repeat.  The
+// chain's first MFMA goes out before any VALU, so work that depends on the
+// previous chain's result cannot hold back the matrix core.
+template <int NS, int V>
+__device__ inline void interleave_mfma_valu() {
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // VALU
   }
 }
 
@@ -145,19 +166,23 @@ struct P1Args {
 // row statistics (max in log2 units, sum of 2^(z - max)) of every query row.
 //
 // Per 32-key tile a wave runs NT chains of 8 MFMAs (one per stationary
-// query tile).  The exp/sum of chain i-1 is issued in the same basic block
-// as the MFMAs of chain i, so the transcendental work runs while the matrix
-// core is busy.  The running maximum is only raised when a tile's sum of
-// 2^(z - m) exceeds 2^64 (first visible tile, or a big jump): the common
-// case costs one FMA, one exp and one add per logit.
+// query tile).  The online-softmax update of chain i-1 (tile max, one FMA,
+// one exp and one add per logit, one rescale per row) is issued between the
+// MFMAs of chain i; a tile is one branch-free basic block, either unmasked
+// (every lane sees all 32 keys) or masked per element.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
   using G_ = Geo<T, D>;
   using MM = Mma<T>;
   using frag = typename MM::frag;
-  constexpr int NT = G_::NT1, NS = G_::NS, ROWB = G_::ROWB, LS = G_::LS, E = G_::E;
-  constexpr int QB = 4 * NT * 32;  // query rows per block
-  __shared__ __attribute__((aligned(16))) char smem[2][kStage * LS];
+  constexpr int NT = G_::NT1, NS = G_::NS, ROWB = G_::ROWB, E = G_::E;
+  constexpr int QB = 4 * NT * 32;      // query rows per block
+  constexpr int KS = kStage1;          // keys per LDS stage
+  static_assert(NT % 2 == 0, "accumulators alternate between two register sets");
+  // two stage buffers as distinct objects, so the compiler can tell the
+  // buffer being read from the one the in-flight DMA writes
+  __shared__ __attribute__((aligned(16))) char smA[KS * ROWB];
+  __shared__ __attribute__((aligned(16))) char smB[KS * ROWB];
 
   // Blocks that share one key chunk (the nqb query blocks of a unit) get
   // ids that are equal mod 8, i.e. land on one XCD and share its L2.
@@ -181,7 +206,8 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
   if (s0 + kbeg > bmax) return;                  // chunk starts after every row of the block
   const int kstop = min(kend, bmax - s0 + 1);    // keys after the last row are never visible
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
   const int hi = lane >> 5, col = lane & 31;
   const int wr0 = row0 + wave * NT * 32;
   const bool active = wr0 < R;
@@ -216,117 +242,119 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
   const float cl2e = a.cl2e;
 
   // keys of one stage, rows clamped into the chunk (rows past kend are masked)
-  auto issue_stage = [&](int ks, int bufi) {
-    dma_stage<T, D>(smem[bufi], wave, lane, [&](int row) {
-      const int key = min(ks + row, kend - 1);
-      return a.k + ((size_t)(s0 + key) * a.Hkv + g) * ROWB;
+  const char *kbase = a.k + ((size_t)s0 * a.Hkv + g) * ROWB;  // key 0 of this sequence, head g
+  const uint32_t kstride = (uint32_t)a.Hkv * ROWB;
+  auto issue_stage = [&](int ks, char *dst) __attribute__((always_inline)) {
+    dma_stage<T, D, KS>(dst, kbase, wave, lane, [&](int row) __attribute__((always_inline)) {
+      return (uint32_t)min(ks + row, kend - 1) * kstride;
     });
   };
 
   // Accumulator element e of this lane holds key kb + hi*4 + eoff(e) of its
-  // query column; it is visible iff eoff(e) <= vlim, with the per-lane limit
-  // vlim = min(q - kb, kend - 1 - kb) - hi*4 (causal row and chunk end).
-  auto eoff = [](int e) { return 8 * (e >> 2) + (e & 3); };
-  auto vlimit = [&](int qi, int kb) { return min(qrel[qi] - kb, kend - 1 - kb) - hi * 4; };
+  // query column; it is visible iff eoff(e) <= vl, with the per-lane limit
+  // vl = min(q - kb, kend - 1 - kb) - hi*4 (causal row and chunk end).
+  auto eoff = [](int e) __attribute__((always_inline)) { return 8 * (e >> 2) + (e & 3); };
+  auto vlimit = [&](int qi, int kb) __attribute__((always_inline)) { return min(qrel[qi] - kb, kend - 1 - kb) - hi * 4; };
+  auto lane_all = [&](int qi, int kb) __attribute__((always_inline)) { return qrel[qi] - kb >= 31 && kb + 32 <= kend; };
+  auto lane_none = [&](int qi, int kb) __attribute__((always_inline)) { return qrel[qi] < kb; };
 
-  // Exact update of row qi with tile kb (any visibility pattern; raises the max).
-  auto exact_update = [&](const f32x16 &acc, int qi, int kb) {
-    const int vl = vlimit(qi, kb);
-    float tm = -INFINITY;
+  // Two accumulator sets: chain qi writes accA (qi even) or accB (qi odd)
+  // while the update of the other one (chain qi-1) runs; accB = -inf means
+  // nothing is pending.
+  f32x16 accA = f32x16{}, accB;
 #pragma unroll
-    for (int e = 0; e < 16; ++e)
-      if (eoff(e) <= vl) tm = fmaxf(tm, acc[e] * cl2e);
-    if (tm == -INFINITY) return;
-    const float nm = fmaxf(m2[qi], tm);
-    float ns = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float x = __builtin_amdgcn_exp2f(acc[e] * cl2e - nm);
-      ns += eoff(e) <= vl ? x : 0.f;
-    }
-    l[qi] = l[qi] * __builtin_amdgcn_exp2f(m2[qi] - nm) + ns;
-    m2[qi] = nm;
-  };
+  for (int e = 0; e < 16; ++e) accB[e] = -INFINITY;
+  int pend_kb = 1 << 30;  // no lane sees the (empty) pending tile
 
-  f32x16 pacc = f32x16{};  // accumulators waiting for their exp/sum
-  int pend_kb = 0;
-  bool pend = false;
-
-  const int nstage = (kstop - kbeg + kStage - 1) / kStage;
-  issue_stage(kbeg, 0);
-  for (int st = 0; st < nstage; ++st) {
-    const int ks = kbeg + st * kStage;
+  const int nstage = (kstop - kbeg + KS - 1) / KS;
+  issue_stage(kbeg, smA);
+  auto step = [&](const char *buf, char *nxt, int st) __attribute__((always_inline)) {
+    const int ks = kbeg + st * KS;
     wait_vmem();
     __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
-    if (st + 1 < nstage) issue_stage(ks + kStage, (st + 1) & 1);
-    const char *buf = smem[st & 1];
+    if (st + 1 < nstage) issue_stage(ks + KS, nxt);
     if (active) {
 #pragma unroll
-      for (int kt = 0; kt < kStage / 32; ++kt) {
+      for (int kt = 0; kt < KS / 32; ++kt) {
         const int kb = ks + kt * 32;  // first key (relative) of this 32-key tile
         if (kb < kstop && s0 + kb <= wmax) {
+          // The pending updates of this tile are (NT-1, pend_kb), (0, kb) ..
+          // (NT-2, kb).  The unmasked block handles lanes that see all 32 keys
+          // of their pending tile or none of them (per-lane selects on the
+          // tile max and sum); a lane that sees only part of one sends the
+          // whole wave through the per-element masked block.
+          bool whole = lane_none(NT - 1, pend_kb) || lane_all(NT - 1, pend_kb);
+#pragma unroll
+          for (int qi = 0; qi + 1 < NT; ++qi) whole = whole && (lane_none(qi, kb) || lane_all(qi, kb));
+          const bool fast = __ballot(!whole) == 0ull;
           frag av[NS];
 #pragma unroll
           for (int s = 0; s < NS; ++s)
             av[s] = load_frag<frag>(buf + swz_off<T, D>(kt * 32 + col, s * 2 * E + hi * E));
+          // one branch-free block per tile: masked (per element) or not
+          auto tile = [&](auto masked_tag) __attribute__((always_inline)) {
+            constexpr bool MASKED = decltype(masked_tag)::value;
 #pragma unroll
-          for (int qi = 0; qi < NT; ++qi) {
-            const int pqi = qi == 0 ? NT - 1 : qi - 1;
-            const int pkb = qi == 0 ? pend_kb : kb;
-            const bool has = qi > 0 || pend;
-            // visibility of the pending tile for this lane: all, none, or partial
-            const int vl = vlimit(pqi, pkb);
-            const bool none = qrel[pqi] - pkb < 0;
-            const bool all = qrel[pqi] - pkb >= 31 && pkb + 32 <= kend;
-            const bool fast = __ballot(!(none || all)) == 0ull;
-            f32x16 acc = f32x16{};
-            float ts = 0.f;
-            if (has && fast) {
+            for (int qi = 0; qi < NT; ++qi) {
+              f32x16 &cur = (qi & 1) ? accB : accA;
+              f32x16 &prv = (qi & 1) ? accA : accB;
+              const int pqi = qi == 0 ? NT - 1 : qi - 1;
+              if (MASKED) {
+                const int vl = vlimit(pqi, qi == 0 ? pend_kb : kb);
+#pragma unroll
+                for (int e = 0; e < 16; ++e) prv[e] = eoff(e) <= vl ? prv[e] : -INFINITY;
+              }
+              // lanes that see none of the pending tile keep their statistics
+              const bool skip = !MASKED && lane_none(pqi, qi == 0 ? pend_kb : kb);
+              float mx = -INFINITY;
+#pragma unroll
+              for (int e = 0; e < 16; ++e) mx = fmaxf(mx, prv[e]);
+              if (skip) mx = -INFINITY;
+              const float nm = fmaxf(m2[pqi], mx * cl2e);
+              const float ref = nm == -INFINITY ? 0.f : nm;
+              cur = f32x16{};
+              float ts = 0.f;
 #pragma unroll
               for (int s = 0; s < NS; ++s) {
-                acc = MM::run(av[s], qf[qi][s], acc);
+                cur = MM::run(av[s], qf[qi][s], cur);
 #pragma unroll
                 for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e)
-                  ts += __builtin_amdgcn_exp2f(pacc[e] * cl2e - m2[pqi]);
+                  ts += __builtin_amdgcn_exp2f(prv[e] * cl2e - ref);
               }
-              if (none) ts = 0.f;
-            } else if (has) {
-#pragma unroll
-              for (int s = 0; s < NS; ++s) {
-                acc = MM::run(av[s], qf[qi][s], acc);
-#pragma unroll
-                for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e) {
-                  const float x = __builtin_amdgcn_exp2f(pacc[e] * cl2e - m2[pqi]);
-                  ts += eoff(e) <= vl ? x : 0.f;
-                }
-              }
-            } else {
-#pragma unroll
-              for (int s = 0; s < NS; ++s) acc = MM::run(av[s], qf[qi][s], acc);
+              if (skip) ts = 0.f;
+              l[pqi] = l[pqi] * __builtin_amdgcn_exp2f(m2[pqi] - ref) + ts;
+              m2[pqi] = nm;
+              interleave_mfma_valu<NS, (MASKED ? 96 : 64) / NS>();
             }
-            if (has) {
-              if (ts <= 0x1p64f) l[pqi] += ts;
-              else exact_update(pacc, pqi, pkb);  // first visible tile, a jump, or NaN
-            }
-            pacc = acc;
-          }
-          pend = true;
+          };
+          if (fast) tile(std::false_type{});
+          else tile(std::true_type{});
           pend_kb = kb;
         }
       }
     }
+  };
+  for (int st = 0; st < nstage; st += 2) {
+    step(smA, smB, st);
+    if (st + 1 < nstage) step(smB, smA, st + 1);
   }
   if (!active) return;
-  if (pend) {
+  {  // last pending update (row NT-1 of the last tile, in accB); no-op if nothing is pending
     const int vl = vlimit(NT - 1, pend_kb);
-    float ts = 0.f;
+    float v[16];
+    float mx = -INFINITY;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const float x = __builtin_amdgcn_exp2f(pacc[e] * cl2e - m2[NT - 1]);
-      ts += eoff(e) <= vl ? x : 0.f;
+      v[e] = eoff(e) <= vl ? accB[e] : -INFINITY;
+      mx = fmaxf(mx, v[e]);
     }
-    if (ts <= 0x1p64f) l[NT - 1] += ts;
-    else exact_update(pacc, NT - 1, pend_kb);
+    const float nm = fmaxf(m2[NT - 1], mx * cl2e);
+    const float ref = nm == -INFINITY ? 0.f : nm;
+    float ts = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) ts += __builtin_amdgcn_exp2f(v[e] * cl2e - ref);
+    l[NT - 1] = l[NT - 1] * __builtin_amdgcn_exp2f(m2[NT - 1] - ref) + ts;
+    m2[NT - 1] = nm;
   }
   // merge the two half-waves (same query column, disjoint keys) and store
   const size_t HqT = (size_t)a.Hq * a.T_tot;
@@ -374,6 +402,16 @@ __global__ void lse_combine_kernel(const float *__restrict__ part_m, const float
   lse[idx] = (M + __builtin_amdgcn_logf(S)) * kLn2;
 }
 
+// One pass-2 LDS stage: kStage query rows (swizzled), their LSE in log2
+// units, their positions, and the position range of each 32-row half.
+template <int ROWB>
+struct __attribute__((aligned(16))) Stage2 {
+  char q[kStage * ROWB];
+  float lse2[kStage];
+  int pos[kStage];
+  int meta[4];
+};
+
 struct P2Args {
   const char *q, *k;
   const float *lse;
@@ -398,10 +436,8 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   using frag = typename MM::frag;
   constexpr int NKT = G_::NT2, NS = G_::NS, ROWB = G_::ROWB, E = G_::E;
   constexpr int KB = 4 * NKT * 32;  // keys per block
-  __shared__ __attribute__((aligned(16))) char smem[2][kStage * ROWB];
-  __shared__ __attribute__((aligned(16))) float s_lse2[2][kStage];
-  __shared__ __attribute__((aligned(16))) int s_pos[2][kStage];
-  __shared__ int s_meta[2][4];  // per 32-row half: min and max position
+  // two stage buffers as distinct objects (see pass 1)
+  __shared__ Stage2<ROWB> stA, stB;
 
   // the nkb key blocks of one (sequence, key head) read the same queries:
   // keep them on one XCD
@@ -418,7 +454,8 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   if (kb0 >= L) return;
   const int32_t *tp = a.text_pos + t0;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
   const int hi = lane >> 5, col = lane & 31;
   const int kw0 = kb0 + wave * NKT * 32;
   const bool active = kw0 < L;
@@ -445,31 +482,32 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   for (int j = 0; j < NKT; ++j) cs[j] = 0.f;
   const float cl2e = a.cl2e;
 
-  auto issue_stage = [&](int rs, int bufi) {
-    dma_stage<T, D>(smem[bufi], wave, lane, [&](int row) {
+  const char *qbase = a.q + ((size_t)t0 * a.Hq + g * a.G) * ROWB;  // text row 0, head g*G
+  auto issue_stage = [&](int rs, Stage2<ROWB> &dst) __attribute__((always_inline)) {
+    dma_stage<T, D, kStage>(dst.q, qbase, wave, lane, [&](int row) __attribute__((always_inline)) {
       const int r = min(rs + row, R - 1);  // padding rows re-read row R-1; their lse is +inf
       const int hh = r / Tb, t = r - hh * Tb;
-      return a.q + ((size_t)(t0 + t) * a.Hq + g * a.G + hh) * ROWB;
+      return (uint32_t)(t * a.Hq + hh) * ROWB;
     });
   };
   float pre_lse = INFINITY;
   int pre_pos = -1;
-  auto load_meta = [&](int rs) {  // wave 0: LSE (log2 units) and position of each row
+  auto load_meta = [&](int rs) __attribute__((always_inline)) {  // wave 0: LSE (log2 units) and position of each row
     if (wave == 0) {
       const int r = rs + lane;
       pre_lse = INFINITY;
       pre_pos = -1;
       if (r < R) {
         const int hh = r / Tb, t = r - hh * Tb;
-        pre_lse = a.lse[(size_t)(g * a.G + hh) * a.T_tot + t0 + t] * kLog2e;
+        pre_lse = a.lse[(size_t)(g * a.G + hh) * a.T_tot + t0 + t];  // scaled at the store
         pre_pos = tp[t];
       }
     }
   };
-  auto store_meta = [&](int bufi) {
+  auto store_meta = [&](Stage2<ROWB> &dst) __attribute__((always_inline)) {
     if (wave == 0) {
-      s_lse2[bufi][lane] = pre_lse;
-      s_pos[bufi][lane] = pre_pos;
+      dst.lse2[lane] = pre_lse * kLog2e;
+      dst.pos[lane] = pre_pos;
       int vmin = pre_pos >= 0 ? pre_pos : 0x7fffffff, vmax = pre_pos;
 #pragma unroll
       for (int off = 16; off > 0; off >>= 1) {  // reduce within each 32-lane half
@@ -477,13 +515,13 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
         vmax = max(vmax, __shfl_xor(vmax, off));
       }
       if (col == 0) {
-        s_meta[bufi][2 * hi] = vmin;
-        s_meta[bufi][2 * hi + 1] = vmax;
+        dst.meta[2 * hi] = vmin;
+        dst.meta[2 * hi + 1] = vmax;
       }
     }
   };
 
-  auto exp_sum = [&](const f32x16 &acc, const float *lv) {
+  auto exp_sum = [&](const f32x16 &acc, const float *lv) __attribute__((always_inline)) {
     float t = 0.f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) t += __builtin_amdgcn_exp2f(acc[e] * cl2e - lv[e]);
@@ -498,34 +536,33 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
 
   const int nstage = (R + kStage - 1) / kStage;
   if (nstage > 0) {
-    issue_stage(0, 0);
+    issue_stage(0, stA);
     load_meta(0);
-    store_meta(0);
+    store_meta(stA);
   }
-  for (int st = 0; st < nstage; ++st) {
+  auto step = [&](Stage2<ROWB> &cur, Stage2<ROWB> &nxt, int st) __attribute__((always_inline)) {
     const int rs = st * kStage;
-    const int bi = st & 1;
     wait_vmem();
     __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
     if (st + 1 < nstage) {
-      issue_stage(rs + kStage, bi ^ 1);
+      issue_stage(rs + kStage, nxt);
       load_meta(rs + kStage);
     }
     if (active) {
 #pragma unroll
       for (int sub = 0; sub < kStage / 32; ++sub) {
         if (rs + sub * 32 >= R) break;
-        const int qmin = s_meta[bi][2 * sub], qmax = s_meta[bi][2 * sub + 1];
+        const int qmin = cur.meta[2 * sub], qmax = cur.meta[2 * sub + 1];
         if (qmax < kmin) continue;  // no row of this tile sees any key of the wave
         frag av[NS];
 #pragma unroll
         for (int s = 0; s < NS; ++s)
-          av[s] = load_frag<frag>(smem[bi] + swz_off<T, D>(sub * 32 + col, s * 2 * E + hi * E));
+          av[s] = load_frag<frag>(cur.q + swz_off<T, D>(sub * 32 + col, s * 2 * E + hi * E));
         // lane's rows: sub*32 + hi*4 + 8*(e/4) + e%4
         float lv[16];
 #pragma unroll
         for (int e4 = 0; e4 < 4; ++e4) {
-          const float4 v = *reinterpret_cast<const float4 *>(&s_lse2[bi][sub * 32 + hi * 4 + 8 * e4]);
+          const float4 v = *reinterpret_cast<const float4 *>(&cur.lse2[sub * 32 + hi * 4 + 8 * e4]);
           lv[4 * e4 + 0] = v.x;
           lv[4 * e4 + 1] = v.y;
           lv[4 * e4 + 2] = v.z;
@@ -547,6 +584,7 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
                   ts += __builtin_amdgcn_exp2f(pacc[e] * cl2e - pl[e]);
               }
               cs[j > 0 ? j - 1 : NKT - 1] += ts;
+              interleave_mfma_valu<NS, 48 / NS>();
             } else {
 #pragma unroll
               for (int s = 0; s < NS; ++s) acc = MM::run(av[s], kf[j][s], acc);
@@ -565,7 +603,7 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
           int qp[16];
 #pragma unroll
           for (int e4 = 0; e4 < 4; ++e4) {
-            const int4 v = *reinterpret_cast<const int4 *>(&s_pos[bi][sub * 32 + hi * 4 + 8 * e4]);
+            const int4 v = *reinterpret_cast<const int4 *>(&cur.pos[sub * 32 + hi * 4 + 8 * e4]);
             qp[4 * e4 + 0] = v.x;
             qp[4 * e4 + 1] = v.y;
             qp[4 * e4 + 2] = v.z;
@@ -587,7 +625,11 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
         }
       }
     }
-    if (st + 1 < nstage) store_meta(bi ^ 1);
+    if (st + 1 < nstage) store_meta(nxt);
+  };
+  for (int st = 0; st < nstage; st += 2) {
+    step(stA, stB, st);
+    if (st + 1 < nstage) step(stB, stA, st + 1);
   }
   if (!active) return;
   if (pend) cs[NKT - 1] += exp_sum(pacc, plv);
