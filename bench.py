@@ -40,7 +40,37 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB mebibytes (counter calibration)")
     return ap.parse_args()
+
+
+def source_digest(path):
+    import hashlib
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload, src_path):
+    """HBM bytes per launch of `kernel` on `workload` from the committed counter
+    summary (profiles/hbm_traffic.txt), or None if absent or taken on other source.
+
+    Each line: kernel workload fetch_kib=F write_kib=W copy_read=R copy_write=C src=SHA
+    where R and C are FETCH_SIZE / WRITE_SIZE divided by the true bytes of a plain copy.
+    """
+    path = os.path.join(HERE, "profiles", "hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    want = source_digest(src_path)
+    for line in open(path):
+        f = line.split()
+        if len(f) < 3 or f[0] != kernel or f[1] != workload:
+            continue
+        kv = dict(x.split("=", 1) for x in f[2:] if "=" in x)
+        if kv.get("src") != want:
+            return None
+        return (float(kv["fetch_kib"]) * 1024 / float(kv["copy_read"])
+                + float(kv["write_kib"]) * 1024 / float(kv["copy_write"]))
+    return None
 
 
 def algorithmic_counts(lay, Hq, d, row_bytes_total):
@@ -66,9 +96,9 @@ def algorithmic_counts(lay, Hq, d, row_bytes_total):
     return flops1, flops2, comp_bytes, sel_bytes
 
 
-def cpu_baseline(wl):
-    """The float64 oracle on one sequence of the workload (score, budget,
-    select, compaction of that sequence's hidden states)."""
+def cpu_baseline(wl, nseq=3):
+    """The float64 oracle on the first `nseq` sequences of the workload (score,
+    budget, select, compaction of those sequences' hidden states)."""
     from oracle import avtp_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -76,32 +106,50 @@ def cpu_baseline(wl):
     except Exception:  # noqa: BLE001
         threads = os.cpu_count() or 1
     lay = wl.layout
-    b = 0
-    t0 = time.perf_counter()
-    s, isum, _, _ = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale, wl.dtype,
-                                  seqs=[b])
-    i0, i1 = int(lay.cu_img[b]), int(lay.cu_img[b + 1])
-    # budget and selection of sequence b only
     from paper_2608_26806_amd.workloads import Layout
-    s0, s1 = int(lay.cu_seqlens[b]), int(lay.cu_seqlens[b + 1])
-    ta, tb = int(lay.cu_text[b]), int(lay.cu_text[b + 1])
-    sub = Layout(np.array([0, s1 - s0], np.int32), (lay.img_start[i0:i1] - s0).astype(np.int32),
-                 lay.img_len[i0:i1].copy(), np.array([0, i1 - i0], np.int32),
-                 (lay.text_pos[ta:tb] - s0).astype(np.int32), np.array([0, tb - ta], np.int32),
-                 lay.keep_total[b:b + 1].copy())
-    bud = O.budget(sub, isum[i0:i1].astype(np.float32), wl.alpha, wl.lo_permille, wl.hi_permille,
-                   wl.floor_abs)
-    keep, _ = O.select(sub, s[s0:s1].astype(np.float32), bud)
-    O.compact(keep, wl.hidden_states[s0:s1])
+    nseq = min(nseq, lay.B)
+    t0 = time.perf_counter()
+    m_tot = t_tot = 0
+    for b in range(nseq):
+        s, isum, _, _ = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale,
+                                      wl.dtype, seqs=[b])
+        i0, i1 = int(lay.cu_img[b]), int(lay.cu_img[b + 1])
+        s0, s1 = int(lay.cu_seqlens[b]), int(lay.cu_seqlens[b + 1])
+        ta, tb = int(lay.cu_text[b]), int(lay.cu_text[b + 1])
+        sub = Layout(np.array([0, s1 - s0], np.int32), (lay.img_start[i0:i1] - s0).astype(np.int32),
+                     lay.img_len[i0:i1].copy(), np.array([0, i1 - i0], np.int32),
+                     (lay.text_pos[ta:tb] - s0).astype(np.int32), np.array([0, tb - ta], np.int32),
+                     lay.keep_total[b:b + 1].copy())
+        bud = O.budget(sub, isum[i0:i1].astype(np.float32), wl.alpha, wl.lo_permille,
+                       wl.hi_permille, wl.floor_abs)
+        keep, _ = O.select(sub, s[s0:s1].astype(np.float32), bud)
+        O.compact(keep, wl.hidden_states[s0:s1])
+        m_tot += int(lay.img_len[i0:i1].sum())
+        t_tot += tb - ta
     dt = time.perf_counter() - t0
-    m = int(lay.img_len[i0:i1].sum())
-    return {"value": m / dt, "unit": "visual tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"sequence 0 of the workload ({m} visual tokens, {tb - ta} text rows), "
+    return {"value": m_tot / dt, "unit": "visual tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {nseq} of {lay.B} sequences ({m_tot} visual tokens, {t_tot} text rows), "
                       f"all four stages, float64 numpy; {dt:.2f} s"}
+
+
+def calibrate_copy(mib):
+    """A plain device-to-device copy of a known size (reads and writes `mib` MiB),
+    run under rocprofv3 to relate FETCH_SIZE / WRITE_SIZE to true bytes."""
+    import torch
+    n = mib * (1 << 20)
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration_copy_bytes": n, "dispatches": 3}))
 
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
                                    "(the per-sequence path shards over sequences, see DESIGN.md)"}))
@@ -224,10 +272,15 @@ def main():
         "us_per_call": {n: ms[n] * 1e3 for n in names},
         "visual_tokens_scored_per_s": M / ((ms["row_lse"] + ms["score"]) * 1e-3),
         "roofline": {
-            "kernel": "pass 1: row statistics (rowstats + lse combine)" if dom == "row_lse"
-                      else "pass 2: column sums (colsum + finalize)",
+            "kernel": "rowstats_kernel (pass 1: row statistics; timed with its lse combine)"
+                      if dom == "row_lse" else
+                      "colsum_kernel (pass 2: column sums; timed with its finalize)",
             "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-            "frac": ach / peak, "traffic": None},
+            "frac": ach / peak,
+            "traffic": measured_traffic("rowstats_kernel" if dom == "row_lse" else "colsum_kernel",
+                                        f"config{args.config}",
+                                        os.path.join(HERE, "paper_2608_26806_amd", "csrc",
+                                                     "score_attn.hip"))},
         "score_passes": {
             "pass1_alg_gflop": f1 / 1e9, "pass1_tflops": tf1, "pass1_frac": tf1 / peak,
             "pass2_alg_gflop": f2 / 1e9, "pass2_tflops": tf2, "pass2_frac": tf2 / peak,
