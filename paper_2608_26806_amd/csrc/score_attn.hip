@@ -39,6 +39,9 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kThreads = 256;  // 4 waves per block in both passes
 constexpr int kStage = 64;     // query rows per LDS stage in pass 2
 constexpr int kStage1 = 128;   // key rows per LDS stage in pass 1
+// A chain of 16 exp2 terms above this means the lazily kept reference of a
+// row is too far below the row's logits: that chain is redone exactly.
+constexpr float kLazyLimit = 18446744073709551616.f;  // 2^64
 
 template <typename T>
 struct Mma;
@@ -59,14 +62,17 @@ struct Mma<float> {
   }
 };
 
-// Register budget, two waves per SIMD (256 VGPRs per wave).  Pass 1: the
-// stationary queries take at most 128 (4 tiles of 32 rows), leaving room for
-// the key fragments and two 16-register accumulator sets.  Pass 2: the
-// stationary keys take at most 96, leaving room for the streamed tile's LSE.
+// Register budget, two waves per SIMD (256 VGPRs per wave).  Pass 1 keeps
+// two 32-row query tiles per wave and four accumulator sets.  Pass 2: the
+// stationary keys take at most 96 registers.
+constexpr int kTiles1 = 2;
+template <typename T>
+struct Occ1 {
+  static constexpr int value = 2;
+};
 __host__ __device__ constexpr int tiles_cap(int budget, int row_bytes, int cap) {
   return (budget / (row_bytes / 8)) > cap ? cap : (budget / (row_bytes / 8));
 }
-__host__ __device__ constexpr int tiles_pass1(int row_bytes) { return tiles_cap(128, row_bytes, 4); }
 __host__ __device__ constexpr int tiles_pass2(int row_bytes) { return tiles_cap(96, row_bytes, 4); }
 
 template <typename T, int D>
@@ -75,7 +81,6 @@ struct Geo {
   static constexpr int NS = D / (2 * E);          // k-steps per 32x32 tile
   static constexpr int ROWB = D * (int)sizeof(T);  // bytes of one head row
   static constexpr int LS = ROWB + 16;             // padded LDS row stride (conflict-free b128 reads)
-  static constexpr int NT1 = tiles_pass1(ROWB);   // stationary 32-row tiles per wave, pass 1
   static constexpr int NT2 = tiles_pass2(ROWB);   // same for pass 2
   static constexpr int V16 = kStage * ROWB / 16 / kThreads;  // 16-byte loads per thread per stage
   static constexpr int V16_ROW = ROWB / 16;
@@ -119,6 +124,51 @@ __device__ inline void dma_stage(char *lds, const char *base, int wave, int lane
   }
 }
 
+// Lane part of the source offsets of a dma_stage whose rows are consecutive
+// with a uniform stride: load i of a wave reads row wave*ROWS/4 + i*RPL +
+// lane/NCH, chunk (lane%NCH) ^ (row & SWZ); the row bits that reach the
+// swizzle repeat with period PER in i, so PER lane offsets cover every load.
+template <typename T, int D, int ROWS>
+struct DmaPlan {
+  using G_ = Geo<T, D>;
+  static constexpr int NCH = G_::NCH;
+  static constexpr int RPL = 64 / NCH;                     // rows per wave load
+  static constexpr int DMA = ROWS * NCH / 64 / 4;          // loads per wave
+  static constexpr int SPAN = G_::SWZ + 1;
+  static constexpr int PER0 = RPL >= SPAN ? 1 : SPAN / RPL;
+  static constexpr int PER = PER0 < DMA ? PER0 : DMA;
+  static_assert(NCH <= 64 && (ROWS / 4) % SPAN == 0, "wave row blocks must align to the swizzle");
+  __device__ static inline void lane_offsets(uint32_t (&lo)[PER], int lane, uint32_t stride) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int r = j * RPL + lane / NCH;
+      lo[j] = (uint32_t)(lane / NCH) * stride + (uint32_t)(((lane % NCH) ^ (r & G_::SWZ)) * 16);
+    }
+  }
+  // rows [0, ROWS) from `base` (row 0) with stride `stride` bytes.  The
+  // wave index and lane offsets are made opaque so that the per-load
+  // constants are rebuilt here (a few scalar ops) instead of being kept live
+  // across the whole loop.
+  __device__ static inline void issue(char *lds, const char *base, int wave, const uint32_t (&lo)[PER],
+                                      uint32_t stride) {
+    int w = wave;
+    asm volatile("" : "+s"(w));
+    uint32_t l[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      l[j] = lo[j];
+      asm volatile("" : "+v"(l[j]));
+    }
+#pragma unroll
+    for (int i = 0; i < DMA; ++i) {
+      const int gi = w * DMA + i;
+      const char *row = base + (uint32_t)(w * (ROWS / 4) + i * RPL) * stride;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(row + l[i % PER]),
+                                       (__attribute__((address_space(3))) void *)(lds + gi * 1024), 16, 0, 0);
+    }
+  }
+};
+
 // Scheduling hint for one MFMA chain of NS steps sharing a basic block with
 // independent VALU work: issue one MFMA, then up to V VALU ops, repeat.  The
 // chain's first MFMA goes out before any VALU, so work that depends on the
@@ -129,6 +179,22 @@ __device__ inline void interleave_mfma_valu() {
   for (int s = 0; s < NS; ++s) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
     __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // VALU
+  }
+}
+
+// Scheduling hint for one pass-1 key tile: per k-step the NT MFMAs of the
+// step, each followed by up to V VALU ops working on the previous tile, then
+// one LDS read of a later step's fragment.
+template <int NS, int NT, int V>
+__device__ inline void interleave_tile() {
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // VALU
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
   }
 }
 
@@ -163,22 +229,27 @@ struct P1Args {
 };
 
 // Pass 1: per (sequence b, key head g, query block, key chunk), partial
-// row statistics (max in log2 units, sum of 2^(z - max)) of every query row.
+// row statistics of every query row: a reference m (log2 units) and the sum
+// l of 2^(z c log2e - m) over the row's visible keys of the chunk.
 //
-// Per 32-key tile a wave runs NT chains of 8 MFMAs (one per stationary
-// query tile).  The online-softmax update of chain i-1 (tile max, one FMA,
-// one exp and one add per logit, one rescale per row) is issued between the
-// MFMAs of chain i; a tile is one branch-free basic block, either unmasked
-// (every lane sees all 32 keys) or masked per element.
+// Each wave holds two 32-row query tiles.  Per 32-key tile the MFMAs of both
+// tiles advance k-step by k-step, while the VALU turns the two accumulators
+// of the previous key tile into exp2 sums (one FMA, one exp2 and one add per
+// logit), so no instruction waits on a result of the running MFMAs.  The
+// reference of a row is kept lazily: it is raised (and the row's sum
+// rescaled) only when a 16-term chain exceeds 2^64, which the exact
+// recomputation of that chain then resolves.  A tile that some lane sees
+// only in part takes a per-element masked variant.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
+__global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Args a) {
   using G_ = Geo<T, D>;
   using MM = Mma<T>;
   using frag = typename MM::frag;
-  constexpr int NT = G_::NT1, NS = G_::NS, ROWB = G_::ROWB, E = G_::E;
-  constexpr int QB = 4 * NT * 32;      // query rows per block
-  constexpr int KS = kStage1;          // keys per LDS stage
-  static_assert(NT % 2 == 0, "accumulators alternate between two register sets");
+  constexpr int NT = kTiles1, NS = G_::NS, ROWB = G_::ROWB, E = G_::E;
+  constexpr int QB = 4 * NT * 32;  // query rows per block
+  constexpr int KS = kStage1;      // keys per LDS stage
+  constexpr int TPS = KS / 32;     // key tiles per stage
+  static_assert(TPS % 2 == 0, "accumulator sets alternate between consecutive key tiles");
   // two stage buffers as distinct objects, so the compiler can tell the
   // buffer being read from the one the in-flight DMA writes
   __shared__ __attribute__((aligned(16))) char smA[KS * ROWB];
@@ -233,10 +304,10 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
     }
   }
 
-  float m2[NT], l[NT];
+  float ref[NT], l[NT];
 #pragma unroll
   for (int i = 0; i < NT; ++i) {
-    m2[i] = -INFINITY;
+    ref[i] = -INFINITY;
     l[i] = 0.f;
   }
   const float cl2e = a.cl2e;
@@ -244,94 +315,166 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
   // keys of one stage, rows clamped into the chunk (rows past kend are masked)
   const char *kbase = a.k + ((size_t)s0 * a.Hkv + g) * ROWB;  // key 0 of this sequence, head g
   const uint32_t kstride = (uint32_t)a.Hkv * ROWB;
+  using DP = DmaPlan<T, D, KS>;
+  uint32_t dlo[DP::PER];
+  DP::lane_offsets(dlo, lane, kstride);
   auto issue_stage = [&](int ks, char *dst) __attribute__((always_inline)) {
-    dma_stage<T, D, KS>(dst, kbase, wave, lane, [&](int row) __attribute__((always_inline)) {
-      return (uint32_t)min(ks + row, kend - 1) * kstride;
-    });
+    if (ks + KS <= kend) {
+      DP::issue(dst, kbase + (size_t)ks * kstride, wave, dlo, kstride);
+    } else {  // last stage of the chunk: rows past its end re-read row kend-1
+      dma_stage<T, D, KS>(dst, kbase, wave, lane, [&](int row) __attribute__((always_inline)) {
+        return (uint32_t)min(ks + row, kend - 1) * kstride;
+      });
+    }
   };
 
   // Accumulator element e of this lane holds key kb + hi*4 + eoff(e) of its
   // query column; it is visible iff eoff(e) <= vl, with the per-lane limit
   // vl = min(q - kb, kend - 1 - kb) - hi*4 (causal row and chunk end).
   auto eoff = [](int e) __attribute__((always_inline)) { return 8 * (e >> 2) + (e & 3); };
-  auto vlimit = [&](int qi, int kb) __attribute__((always_inline)) { return min(qrel[qi] - kb, kend - 1 - kb) - hi * 4; };
-  auto lane_all = [&](int qi, int kb) __attribute__((always_inline)) { return qrel[qi] - kb >= 31 && kb + 32 <= kend; };
-  auto lane_none = [&](int qi, int kb) __attribute__((always_inline)) { return qrel[qi] < kb; };
+  auto vlimit = [&](int qi, int kb) __attribute__((always_inline)) {
+    return min(qrel[qi] - kb, kend - 1 - kb) - hi * 4;
+  };
 
-  // Two accumulator sets: chain qi writes accA (qi even) or accB (qi odd)
-  // while the update of the other one (chain qi-1) runs; accB = -inf means
-  // nothing is pending.
-  f32x16 accA = f32x16{}, accB;
+  // Accumulator sets: the key tile of parity p is computed into acc[p*NT ..]
+  // while the other parity's sets hold the pending tile at key pend_kb.
+  f32x16 acc[2 * NT];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) accB[e] = -INFINITY;
-  int pend_kb = 1 << 30;  // no lane sees the (empty) pending tile
+  for (int i = 0; i < 2 * NT; ++i) acc[i] = f32x16{};
+  constexpr int kNone = 1 << 30;  // pend_kb of an empty pending tile: no lane sees it
+  int pend_kb = kNone;
+
+  // One key tile: MFMAs of the tile at buf row `lrow` into the sets of
+  // parity P (if MF), and the exp2 sums of the pending tile (sets of parity
+  // P^1), unmasked (every lane sees all or none of it) or per element.
+  auto tile = [&](const char *buf, int lrow, auto par_tag, auto masked_tag, auto mf_tag)
+      __attribute__((always_inline)) {
+    constexpr int P = decltype(par_tag)::value;
+    constexpr bool MASKED = decltype(masked_tag)::value;
+    constexpr bool MF = decltype(mf_tag)::value;
+    constexpr int CS = P * NT, PS = (P ^ 1) * NT;
+    int vl[NT];
+    float r[NT], ts[NT][2];
+#pragma unroll
+    for (int qi = 0; qi < NT; ++qi) {
+      vl[qi] = vlimit(qi, pend_kb);
+      r[qi] = ref[qi];
+      ts[qi][0] = 0.f;
+      ts[qi][1] = 0.f;
+    }
+    if (MF) {
+#pragma unroll
+      for (int qi = 0; qi < NT; ++qi) acc[CS + qi] = f32x16{};
+    }
+    // key fragments are read PF k-steps ahead of their MFMAs
+    constexpr int PF = NS < 3 ? NS : 3;
+    frag av[NS];
+    if (MF) {
+#pragma unroll
+      for (int s = 0; s < PF; ++s)
+        av[s] = load_frag<frag>(buf + swz_off<T, D>(lrow + col, s * 2 * E + hi * E));
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      if (MF) {
+        if (s + PF < NS)
+          av[s + PF] = load_frag<frag>(buf + swz_off<T, D>(lrow + col, (s + PF) * 2 * E + hi * E));
+#pragma unroll
+        for (int qi = 0; qi < NT; ++qi) acc[CS + qi] = MM::run(av[s], qf[qi][s], acc[CS + qi]);
+      }
+#pragma unroll
+      for (int qi = 0; qi < NT; ++qi) {
+#pragma unroll
+        for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e) {
+          float x = acc[PS + qi][e];
+          if (MASKED) x = eoff(e) <= vl[qi] ? x : -INFINITY;
+          ts[qi][e & 1] += __builtin_amdgcn_exp2f(x * cl2e - r[qi]);
+        }
+      }
+    }
+    if (MF) interleave_tile<NS, NT, ((MASKED ? 64 : 48) / NS > 0 ? (MASKED ? 64 : 48) / NS : 1)>();
+    float t[NT];
+    bool bad = false;
+#pragma unroll
+    for (int qi = 0; qi < NT; ++qi) {
+      t[qi] = ts[qi][0] + ts[qi][1];
+      if (!MASKED && vl[qi] < 0) t[qi] = 0.f;  // lane sees none of the pending tile
+      bad = bad || !(t[qi] <= kLazyLimit);
+    }
+    if (__ballot(bad) != 0ull) {
+      // exact redo of the chains whose sum left the range: raise the
+      // reference to the chain's maximum and rescale the row sum
+#pragma unroll
+      for (int qi = 0; qi < NT; ++qi) {
+        if (!(t[qi] <= kLazyLimit)) {
+          float mx = -INFINITY;
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (eoff(e) <= vl[qi]) mx = fmaxf(mx, acc[PS + qi][e]);
+          const float nm = fmaxf(ref[qi], mx * cl2e);
+          float u = 0.f;
+          if (nm != -INFINITY) {
+            l[qi] = ref[qi] == -INFINITY ? 0.f : l[qi] * __builtin_amdgcn_exp2f(ref[qi] - nm);
+            ref[qi] = nm;
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              if (eoff(e) <= vl[qi]) u += __builtin_amdgcn_exp2f(acc[PS + qi][e] * cl2e - nm);
+          }
+          t[qi] = u;
+        }
+      }
+    }
+#pragma unroll
+    for (int qi = 0; qi < NT; ++qi) l[qi] += t[qi];
+  };
+  using P0 = std::integral_constant<int, 0>;
 
   const int nstage = (kstop - kbeg + KS - 1) / KS;
+  // key tiles this wave processes: those below kstop that start at or
+  // before its last row (a prefix of the chunk's tiles)
+  const int kw_end = active ? min(kstop, wmax - s0 + 1) : kbeg;
+  const int ntw = kw_end > kbeg ? (kw_end - kbeg + 31) / 32 : 0;
   issue_stage(kbeg, smA);
   auto step = [&](const char *buf, char *nxt, int st) __attribute__((always_inline)) {
     const int ks = kbeg + st * KS;
     wait_vmem();
     __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
     if (st + 1 < nstage) issue_stage(ks + KS, nxt);
-    if (active) {
+    if ((st + 1) * TPS <= ntw) {
+      // every tile of the stage is this wave's: no per-tile bounds
+      auto one = [&](auto kt_tag) __attribute__((always_inline)) {
+        constexpr int KT = decltype(kt_tag)::value;
+        using par_tag = std::integral_constant<int, KT & 1>;
+        // a lane that sees only part of the pending tile needs the masked variant
+        bool part = false;
 #pragma unroll
-      for (int kt = 0; kt < KS / 32; ++kt) {
-        const int kb = ks + kt * 32;  // first key (relative) of this 32-key tile
-        if (kb < kstop && s0 + kb <= wmax) {
-          // The pending updates of this tile are (NT-1, pend_kb), (0, kb) ..
-          // (NT-2, kb).  The unmasked block handles lanes that see all 32 keys
-          // of their pending tile or none of them (per-lane selects on the
-          // tile max and sum); a lane that sees only part of one sends the
-          // whole wave through the per-element masked block.
-          bool whole = lane_none(NT - 1, pend_kb) || lane_all(NT - 1, pend_kb);
-#pragma unroll
-          for (int qi = 0; qi + 1 < NT; ++qi) whole = whole && (lane_none(qi, kb) || lane_all(qi, kb));
-          const bool fast = __ballot(!whole) == 0ull;
-          frag av[NS];
-#pragma unroll
-          for (int s = 0; s < NS; ++s)
-            av[s] = load_frag<frag>(buf + swz_off<T, D>(kt * 32 + col, s * 2 * E + hi * E));
-          // one branch-free block per tile: masked (per element) or not
-          auto tile = [&](auto masked_tag) __attribute__((always_inline)) {
-            constexpr bool MASKED = decltype(masked_tag)::value;
-#pragma unroll
-            for (int qi = 0; qi < NT; ++qi) {
-              f32x16 &cur = (qi & 1) ? accB : accA;
-              f32x16 &prv = (qi & 1) ? accA : accB;
-              const int pqi = qi == 0 ? NT - 1 : qi - 1;
-              if (MASKED) {
-                const int vl = vlimit(pqi, qi == 0 ? pend_kb : kb);
-#pragma unroll
-                for (int e = 0; e < 16; ++e) prv[e] = eoff(e) <= vl ? prv[e] : -INFINITY;
-              }
-              // lanes that see none of the pending tile keep their statistics
-              const bool skip = !MASKED && lane_none(pqi, qi == 0 ? pend_kb : kb);
-              float mx = -INFINITY;
-#pragma unroll
-              for (int e = 0; e < 16; ++e) mx = fmaxf(mx, prv[e]);
-              if (skip) mx = -INFINITY;
-              const float nm = fmaxf(m2[pqi], mx * cl2e);
-              const float ref = nm == -INFINITY ? 0.f : nm;
-              cur = f32x16{};
-              float ts = 0.f;
-#pragma unroll
-              for (int s = 0; s < NS; ++s) {
-                cur = MM::run(av[s], qf[qi][s], cur);
-#pragma unroll
-                for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e)
-                  ts += __builtin_amdgcn_exp2f(prv[e] * cl2e - ref);
-              }
-              if (skip) ts = 0.f;
-              l[pqi] = l[pqi] * __builtin_amdgcn_exp2f(m2[pqi] - ref) + ts;
-              m2[pqi] = nm;
-              interleave_mfma_valu<NS, (MASKED ? 96 : 64) / NS>();
-            }
-          };
-          if (fast) tile(std::false_type{});
-          else tile(std::true_type{});
-          pend_kb = kb;
+        for (int qi = 0; qi < NT; ++qi) part = part || (unsigned)(qrel[qi] - pend_kb) < 31u;
+        if (__ballot(part) == 0ull) tile(buf, KT * 32, par_tag{}, std::false_type{}, std::true_type{});
+        else tile(buf, KT * 32, par_tag{}, std::true_type{}, std::true_type{});
+        pend_kb = ks + KT * 32;
+      };
+      static_assert(TPS == 4, "one stage is four key tiles");
+      one(std::integral_constant<int, 0>{});
+      one(std::integral_constant<int, 1>{});
+      one(std::integral_constant<int, 2>{});
+      one(std::integral_constant<int, 3>{});
+    } else if (st * TPS < ntw) {
+      // the wave's last tiles, then settle the pending one (masked variant)
+      auto one = [&](auto kt_tag) __attribute__((always_inline)) {
+        constexpr int KT = decltype(kt_tag)::value;
+        using par_tag = std::integral_constant<int, KT & 1>;
+        if (st * TPS + KT < ntw) {
+          tile(buf, KT * 32, par_tag{}, std::true_type{}, std::true_type{});
+          pend_kb = ks + KT * 32;
+        } else if (st * TPS + KT == ntw) {
+          tile(buf, 0, par_tag{}, std::true_type{}, std::false_type{});
+          pend_kb = kNone;
         }
-      }
+      };
+      one(std::integral_constant<int, 0>{});
+      one(std::integral_constant<int, 1>{});
+      one(std::integral_constant<int, 2>{});
+      one(std::integral_constant<int, 3>{});
     }
   };
   for (int st = 0; st < nstage; st += 2) {
@@ -339,32 +482,19 @@ __global__ __launch_bounds__(kThreads, 2) void rowstats_kernel(P1Args a) {
     if (st + 1 < nstage) step(smB, smA, st + 1);
   }
   if (!active) return;
-  {  // last pending update (row NT-1 of the last tile, in accB); no-op if nothing is pending
-    const int vl = vlimit(NT - 1, pend_kb);
-    float v[16];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      v[e] = eoff(e) <= vl ? accB[e] : -INFINITY;
-      mx = fmaxf(mx, v[e]);
-    }
-    const float nm = fmaxf(m2[NT - 1], mx * cl2e);
-    const float ref = nm == -INFINITY ? 0.f : nm;
-    float ts = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) ts += __builtin_amdgcn_exp2f(v[e] * cl2e - ref);
-    l[NT - 1] = l[NT - 1] * __builtin_amdgcn_exp2f(m2[NT - 1] - ref) + ts;
-    m2[NT - 1] = nm;
-  }
+  // with a whole number of stages the pending tile is the last (odd) one
+  if (ntw > 0 && ntw % TPS == 0) tile(smA, 0, P0{}, std::true_type{}, std::false_type{});
+
   // merge the two half-waves (same query column, disjoint keys) and store
   const size_t HqT = (size_t)a.Hq * a.T_tot;
 #pragma unroll
   for (int i = 0; i < NT; ++i) {
-    const float om = __shfl_xor(m2[i], 32), ol = __shfl_xor(l[i], 32);
-    const float nm = fmaxf(m2[i], om);
+    const float om = __shfl_xor(ref[i], 32), ol = __shfl_xor(l[i], 32);
+    const float nm = fmaxf(ref[i], om);
     float tot = 0.f;
     if (nm != -INFINITY)
-      tot = l[i] * __builtin_amdgcn_exp2f(m2[i] - nm) + ol * __builtin_amdgcn_exp2f(om - nm);
+      tot = (ref[i] == -INFINITY ? 0.f : l[i] * __builtin_amdgcn_exp2f(ref[i] - nm)) +
+            (om == -INFINITY ? 0.f : ol * __builtin_amdgcn_exp2f(om - nm));
     const int r = wr0 + i * 32 + col;
     if (hi == 0 && r < R) {
       const int hh = r / Tb, qidx = (g * a.G + hh) * a.T_tot + t0 + (r - hh * Tb);
@@ -768,7 +898,7 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   AttnPlan P;
   P.G = Hq / Hkv;
   const int row_bytes = d * (dtype == AVTP_FP32 ? 4 : 2);
-  const int rows_per_block = 4 * tiles_pass1(row_bytes) * 32;  // pass 1 query rows per block
+  const int rows_per_block = 4 * kTiles1 * 32;                 // pass 1 query rows per block
   const int keys_per_block = 4 * tiles_pass2(row_bytes) * 32;  // pass 2 keys per block
   P.rows_max = P.G * L.max_text;
   P.nqb = (P.rows_max + rows_per_block - 1) / rows_per_block;
