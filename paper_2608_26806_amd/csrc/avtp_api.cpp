@@ -168,7 +168,7 @@ int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
   if (e == hipSuccess && L.T_tot > 0)
     e = launch_colsum(st, L, P, dtype, q_text, k, Hq, Hkv, d, softmax_scale, lse, w);
   if (e == hipSuccess)
-    e = launch_finalize(st, L, (const float *)(w + P.off_colsum), Hq, Hkv, scores, img_sum,
+    e = launch_finalize(st, L, (const float *)(w + P.off_colsum), Hq, Hkv * P.nqs, scores, img_sum,
                         status);
   return hip_status(e);
 }

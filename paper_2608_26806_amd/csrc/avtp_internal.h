@@ -27,6 +27,7 @@ struct AttnPlan {
   int kchunk;     // keys per pass-1 chunk (multiple of 64)
   int nkc;        // chunks per sequence (max)
   int nkb;        // key blocks per (sequence, key head) in pass 2
+  int nqs;        // query splits of pass 2 (column-sum planes per key head)
   size_t off_part_m, off_part_l, off_lse, off_colsum, bytes;
 };
 
@@ -40,9 +41,11 @@ hipError_t launch_colsum(hipStream_t stream, const DevLayout &L, const AttnPlan 
                          const void *q, const void *k, int Hq, int Hkv, int d, float scale,
                          const float *row_lse, char *ws);
 // Per-image finalisation shared by both score modes.  colsum == nullptr:
-// scores already hold the per-token values (variation mode).
+// scores already hold the per-token values (variation mode); otherwise the
+// score of token j is the sum of `planes` column-sum planes at j over
+// (Hq * rows after j).
 hipError_t launch_finalize(hipStream_t stream, const DevLayout &L, const float *colsum, int Hq,
-                           int Hkv, float *scores, float *img_sum, int32_t *status);
+                           int planes, float *scores, float *img_sum, int32_t *status);
 hipError_t launch_variation(hipStream_t stream, const DevLayout &L, int dtype, const void *h_cur,
                             const void *h_prior, int hidden, float *scores);
 hipError_t launch_budget(hipStream_t stream, const DevLayout &L, const float *img_sum, int mode,

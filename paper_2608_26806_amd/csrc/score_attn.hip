@@ -37,7 +37,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kThreads = 256;  // 4 waves per block in both passes
-constexpr int kStage = 64;     // query rows per LDS stage in pass 2
+constexpr int kStage = 128;    // query rows per LDS stage in pass 2
 constexpr int kStage1 = 128;   // key rows per LDS stage in pass 1
 // A chain of 16 exp2 terms above this means the lazily kept reference of a
 // row is too far below the row's logits: that chain is redone exactly.
@@ -63,17 +63,17 @@ struct Mma<float> {
 };
 
 // Register budget, two waves per SIMD (256 VGPRs per wave).  Pass 1 keeps
-// two 32-row query tiles per wave and four accumulator sets.  Pass 2: the
-// stationary keys take at most 96 registers.
+// two 32-row query tiles per wave and four accumulator sets; pass 2 keeps up
+// to 96 registers of stationary key tiles, one accumulator set each.
 constexpr int kTiles1 = 2;
 template <typename T>
 struct Occ1 {
   static constexpr int value = 2;
 };
-__host__ __device__ constexpr int tiles_cap(int budget, int row_bytes, int cap) {
-  return (budget / (row_bytes / 8)) > cap ? cap : (budget / (row_bytes / 8));
+// pass 2: stationary key fragments take at most 96 registers
+__host__ __device__ constexpr int tiles_pass2(int row_bytes) {
+  return 96 / (row_bytes / 8) < 1 ? 1 : (96 / (row_bytes / 8) > 4 ? 4 : 96 / (row_bytes / 8));
 }
-__host__ __device__ constexpr int tiles_pass2(int row_bytes) { return tiles_cap(96, row_bytes, 4); }
 
 template <typename T, int D>
 struct Geo {
@@ -532,56 +532,74 @@ __global__ void lse_combine_kernel(const float *__restrict__ part_m, const float
   lse[idx] = (M + __builtin_amdgcn_logf(S)) * kLn2;
 }
 
-// One pass-2 LDS stage: kStage query rows (swizzled), their LSE in log2
-// units, their positions, and the position range of each 32-row half.
+// Pass-2 LDS stage: kStage query rows (swizzled) with their row LSE and
+// positions, double-buffered.  Rows past the end of the split get LSE +inf
+// and position -1, copied from these two constants, so they add nothing and
+// are never visible.
+__device__ const float kRowNone = INFINITY;
+__device__ const int kPosNone = -1;
 template <int ROWB>
-struct __attribute__((aligned(16))) Stage2 {
+struct __attribute__((aligned(16))) QTile2 {
   char q[kStage * ROWB];
-  float lse2[kStage];
+  float lse[kStage];  // natural log
   int pos[kStage];
-  int meta[4];
 };
 
 struct P2Args {
   const char *q, *k;
   const float *lse;
   const int32_t *cu_seqlens, *cu_text, *text_pos;
-  int B, Hq, Hkv, G, T_tot, N_tok, nkb;
+  int B, Hq, Hkv, G, T_tot, N_tok, nkb, nqs;
   float cl2e;
-  float *colsum;  // [Hkv][N_tok]
+  float *colsum;  // [nqs][Hkv][N_tok]
 };
 
-// Pass 2: per (sequence b, key head g, key block), the column sums
-// sum_{h in group g} sum_t exp(c q_{t,h}.k_j - lse[h,t]) over visible rows.
+// Pass 2: per (sequence b, key head g, key block, query split), the column
+// sums sum_{h in group g} sum_t exp(c q_{t,h}.k_j - lse[h,t]) over the split's
+// rows t that see key j.
 //
-// Query tiles (and their LSE, positions and position range) stream through
-// double-buffered LDS; keys are the stationary MFMA operand.  For a 32-row
-// tile that sees every key of the wave, the exp/sum of key tile j-1 is
-// issued between the MFMAs of key tile j; tiles that see only part of the
-// wave's keys take a masked path, tiles that see none are skipped.
+// Keys are the stationary MFMA operand: each wave holds NKT 32-key tiles.
+// Query sub-tiles of 32 rows stream through double-buffered LDS together
+// with their row LSE and positions, all brought in by direct-to-LDS loads.
+// Per sub-tile the wave runs one chain of MFMAs per key tile, chain j into
+// accumulator set j; the VALU work interleaved with chain j turns the
+// accumulators of the chain DIST chains earlier (of this sub-tile or the
+// previous one processed) into exp2 terms, one FMA, one exp2 and one add
+// per logit, so it never waits on a running MFMA.  A sub-tile some rows of
+// which see only part of the wave's keys is done unpipelined with a
+// per-element mask; sub-tiles that see none are skipped.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   using G_ = Geo<T, D>;
   using MM = Mma<T>;
   using frag = typename MM::frag;
   constexpr int NKT = G_::NT2, NS = G_::NS, ROWB = G_::ROWB, E = G_::E;
+  constexpr int DIST = NKT >= 3 ? 2 : NKT - 1;  // pipeline distance in chains
   constexpr int KB = 4 * NKT * 32;  // keys per block
-  // two stage buffers as distinct objects (see pass 1)
-  __shared__ Stage2<ROWB> stA, stB;
+  constexpr int QR = kStage;        // query rows per stage
+  constexpr int SUBS = QR / 32;     // sub-tiles per stage
+  static_assert(SUBS == 4, "one stage is four query sub-tiles");
+  // two query buffers as distinct objects (see pass 1)
+  __shared__ QTile2<ROWB> qtA, qtB;
 
-  // the nkb key blocks of one (sequence, key head) read the same queries:
-  // keep them on one XCD
+  // the key blocks of one (sequence, key head, query split) read the same
+  // queries: keep them on one XCD
   const int nunits = a.B * a.Hkv;
+  const int per = a.nkb * a.nqs;
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-  const int kb = local % a.nkb;
-  const int unit = (local / a.nkb) * 8 + xcd;
+  const int wi = local % per;
+  const int unit = (local / per) * 8 + xcd;
   if (unit >= nunits) return;
+  const int kb = wi % a.nkb, qsp = wi / a.nkb;
   const int g = unit % a.Hkv, b = unit / a.Hkv;
   const int s0 = a.cu_seqlens[b], L = a.cu_seqlens[b + 1] - s0;
   const int t0 = a.cu_text[b], Tb = a.cu_text[b + 1] - t0;
   const int R = a.G * Tb;
   const int kb0 = kb * KB;
   if (kb0 >= L) return;
+  // rows of this split: [r_lo, r_hi), split boundaries on whole stages
+  const int rps = ((R + a.nqs - 1) / a.nqs + QR - 1) / QR * QR;
+  const int r_lo = min(R, qsp * rps), r_hi = min(R, r_lo + rps);
   const int32_t *tp = a.text_pos + t0;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -592,182 +610,220 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   const int kmin = s0 + kw0, kmax = s0 + min(L, kw0 + NKT * 32) - 1;
 
   frag kf[NKT][NS];
-  int kpos[NKT];
 #pragma unroll
   for (int j = 0; j < NKT; ++j) {
     const int key = kw0 + j * 32 + col;
     if (key < L) {
-      kpos[j] = s0 + key;
       const char *src = a.k + ((size_t)(s0 + key) * a.Hkv + g) * ROWB + hi * E * sizeof(T);
 #pragma unroll
       for (int s = 0; s < NS; ++s) kf[j][s] = load_frag<frag>(src + s * 2 * E * sizeof(T));
     } else {
-      kpos[j] = 0x7fffffff;
 #pragma unroll
       for (int s = 0; s < NS; ++s) kf[j][s] = frag{};
     }
   }
+  // position of this lane's key in key tile j (padding keys: never visible)
+  auto kpos = [&](int j) __attribute__((always_inline)) {
+    const int key = kw0 + j * 32 + col;
+    return key < L ? s0 + key : 0x7fffffff;
+  };
   float cs[NKT];
 #pragma unroll
   for (int j = 0; j < NKT; ++j) cs[j] = 0.f;
   const float cl2e = a.cl2e;
 
   const char *qbase = a.q + ((size_t)t0 * a.Hq + g * a.G) * ROWB;  // text row 0, head g*G
-  auto issue_stage = [&](int rs, Stage2<ROWB> &dst) __attribute__((always_inline)) {
-    dma_stage<T, D, kStage>(dst.q, qbase, wave, lane, [&](int row) __attribute__((always_inline)) {
-      const int r = min(rs + row, R - 1);  // padding rows re-read row R-1; their lse is +inf
-      const int hh = r / Tb, t = r - hh * Tb;
-      return (uint32_t)(t * a.Hq + hh) * ROWB;
-    });
-  };
-  float pre_lse = INFINITY;
-  int pre_pos = -1;
-  auto load_meta = [&](int rs) __attribute__((always_inline)) {  // wave 0: LSE (log2 units) and position of each row
-    if (wave == 0) {
-      const int r = rs + lane;
-      pre_lse = INFINITY;
-      pre_pos = -1;
-      if (r < R) {
-        const int hh = r / Tb, t = r - hh * Tb;
-        pre_lse = a.lse[(size_t)(g * a.G + hh) * a.T_tot + t0 + t];  // scaled at the store
-        pre_pos = tp[t];
-      }
+  const uint32_t qstride = (uint32_t)a.Hq * ROWB;
+  const float *lbase = a.lse + (size_t)g * a.G * a.T_tot + t0;     // head g*G, text row 0
+  using DP = DmaPlan<T, D, QR>;
+  // One stage: query rows, their LSE and positions.  Wave 0 loads the LSE,
+  // wave 1 the positions, 64 rows per instruction.
+  auto issue_stage = [&](int rs, QTile2<ROWB> &dst) __attribute__((always_inline)) {
+    const int hh = rs / Tb;
+    const bool one_head = rs + QR <= r_hi && (rs + QR - 1) / Tb == hh;
+    if (one_head) {  // consecutive text rows of one head
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      uint32_t dlo[DP::PER];
+      DP::lane_offsets(dlo, ln, qstride);
+      DP::issue(dst.q, qbase + ((size_t)(rs - hh * Tb) * a.Hq + hh) * ROWB, wave, dlo, qstride);
+    } else {
+      dma_stage<T, D, QR>(dst.q, qbase, wave, lane, [&](int row) __attribute__((always_inline)) {
+        const int r = min(rs + row, R - 1);  // rows past R re-read row R-1; their lse is +inf
+        const int h2 = r / Tb, t = r - h2 * Tb;
+        return (uint32_t)(t * a.Hq + h2) * ROWB;
+      });
     }
-  };
-  auto store_meta = [&](Stage2<ROWB> &dst) __attribute__((always_inline)) {
-    if (wave == 0) {
-      dst.lse2[lane] = pre_lse * kLog2e;
-      dst.pos[lane] = pre_pos;
-      int vmin = pre_pos >= 0 ? pre_pos : 0x7fffffff, vmax = pre_pos;
+    if (wave < 2) {
 #pragma unroll
-      for (int off = 16; off > 0; off >>= 1) {  // reduce within each 32-lane half
-        vmin = min(vmin, __shfl_xor(vmin, off));
-        vmax = max(vmax, __shfl_xor(vmax, off));
-      }
-      if (col == 0) {
-        dst.meta[2 * hi] = vmin;
-        dst.meta[2 * hi + 1] = vmax;
+      for (int i = 0; i < QR / 64; ++i) {
+        const int r = rs + i * 64 + lane;
+        const void *src;
+        if (one_head) {
+          const int t = r - hh * Tb;
+          src = wave == 0 ? (const void *)(lbase + (size_t)hh * a.T_tot + t) : (const void *)(tp + t);
+        } else if (r < r_hi) {
+          const int h2 = r / Tb, t = r - h2 * Tb;
+          src = wave == 0 ? (const void *)(lbase + (size_t)h2 * a.T_tot + t) : (const void *)(tp + t);
+        } else {
+          src = wave == 0 ? (const void *)&kRowNone : (const void *)&kPosNone;
+        }
+        void *dstp = wave == 0 ? (void *)(dst.lse + i * 64) : (void *)(dst.pos + i * 64);
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+                                         (__attribute__((address_space(3))) void *)dstp, 4, 0, 0);
       }
     }
   };
 
-  auto exp_sum = [&](const f32x16 &acc, const float *lv) __attribute__((always_inline)) {
-    float t = 0.f;
+  // acc[j]: chain j of the latest sub-tile processed.  The chains
+  // NKT-DIST .. NKT-1 of the previous sub-tile processed are still pending,
+  // with that sub-tile's LSE (log2 units) in plv (+inf: nothing pending).
+  f32x16 acc[NKT];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) t += __builtin_amdgcn_exp2f(acc[e] * cl2e - lv[e]);
-    return t;
-  };
-
-  f32x16 pacc = f32x16{};
+  for (int j = 0; j < NKT; ++j) acc[j] = f32x16{};
   float plv[16];
 #pragma unroll
   for (int e = 0; e < 16; ++e) plv[e] = INFINITY;
-  bool pend = false;  // pacc holds key tile NKT-1 of an earlier row tile
 
-  const int nstage = (R + kStage - 1) / kStage;
-  if (nstage > 0) {
-    issue_stage(0, stA);
-    load_meta(0);
-    store_meta(stA);
-  }
-  auto step = [&](Stage2<ROWB> &cur, Stage2<ROWB> &nxt, int st) __attribute__((always_inline)) {
-    const int rs = st * kStage;
-    wait_vmem();
-    __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
-    if (st + 1 < nstage) {
-      issue_stage(rs + kStage, nxt);
-      load_meta(rs + kStage);
+  // exp2 terms of chain c (its accumulators in set c) for elements [e0, e1)
+  auto terms = [&](int c, int e0, int e1, const float *lv, float (&ts)[2])
+      __attribute__((always_inline)) {
+#pragma unroll
+    for (int e = e0; e < e1; ++e) ts[e & 1] += __builtin_amdgcn_exp2f(acc[c][e] * cl2e - lv[e]);
+  };
+  // the sub-tile's LSE of this lane's rows, in log2 units
+  auto load_lv = [&](const QTile2<ROWB> &cur, int U, float (&lv)[16]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4) {
+      const float4 x = *reinterpret_cast<const float4 *>(&cur.lse[U * 32 + hi * 4 + 8 * e4]);
+      lv[4 * e4 + 0] = x.x * kLog2e;
+      lv[4 * e4 + 1] = x.y * kLog2e;
+      lv[4 * e4 + 2] = x.z * kLog2e;
+      lv[4 * e4 + 3] = x.w * kLog2e;
     }
-    if (active) {
+  };
+  // a sub-tile in stage slot U that every row of which sees every key of the
+  // wave: chain j of MFMAs with the terms of chain j-DIST in between
+  auto sub_tile = [&](const QTile2<ROWB> &cur, auto u_tag) __attribute__((always_inline)) {
+    constexpr int U = decltype(u_tag)::value;
+    frag av[NS];
 #pragma unroll
-      for (int sub = 0; sub < kStage / 32; ++sub) {
-        if (rs + sub * 32 >= R) break;
-        const int qmin = cur.meta[2 * sub], qmax = cur.meta[2 * sub + 1];
-        if (qmax < kmin) continue;  // no row of this tile sees any key of the wave
-        frag av[NS];
+    for (int s = 0; s < NS; ++s) av[s] = load_frag<frag>(cur.q + swz_off<T, D>(U * 32 + col, s * 2 * E + hi * E));
+    // this sub-tile's LSE, read once the pending chains no longer need plv
+    float clv[16];
 #pragma unroll
-        for (int s = 0; s < NS; ++s)
-          av[s] = load_frag<frag>(cur.q + swz_off<T, D>(sub * 32 + col, s * 2 * E + hi * E));
-        // lane's rows: sub*32 + hi*4 + 8*(e/4) + e%4
-        float lv[16];
+    for (int j = 0; j < NKT; ++j) {
+      if (j == DIST) load_lv(cur, U, clv);
+      const int pj = j - DIST;       // chain processed by the VALU alongside chain j
+      const bool prev = pj < 0;      // (of the previous sub-tile)
+      const int pc = prev ? pj + NKT : pj;
+      float ts[2] = {0.f, 0.f};
+      acc[j] = f32x16{};
+      if (DIST > 0) {
 #pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const float4 v = *reinterpret_cast<const float4 *>(&cur.lse2[sub * 32 + hi * 4 + 8 * e4]);
-          lv[4 * e4 + 0] = v.x;
-          lv[4 * e4 + 1] = v.y;
-          lv[4 * e4 + 2] = v.z;
-          lv[4 * e4 + 3] = v.w;
+        for (int s = 0; s < NS; ++s) {
+          acc[j] = MM::run(av[s], kf[j][s], acc[j]);
+          terms(pc, (s * 16) / NS, ((s + 1) * 16) / NS, prev ? plv : clv, ts);
         }
-        if (qmin >= kmax) {
-          // every row sees every key of the wave: pipelined MFMA + exp/sum
+        interleave_mfma_valu<NS, (48 / NS > 0 ? 48 / NS : 1)>();
+      } else {
 #pragma unroll
-          for (int j = 0; j < NKT; ++j) {
-            f32x16 acc = f32x16{};
-            float ts = 0.f;
-            if (j > 0 || pend) {
-              const float *pl = j > 0 ? lv : plv;
+        for (int s = 0; s < NS; ++s) acc[j] = MM::run(av[s], kf[j][s], acc[j]);
+        terms(pc, 0, 16, clv, ts);
+      }
+      cs[pc] += ts[0] + ts[1];
+    }
+    // the last DIST chains of this sub-tile are now the pending ones
 #pragma unroll
-              for (int s = 0; s < NS; ++s) {
-                acc = MM::run(av[s], kf[j][s], acc);
+    for (int e = 0; e < 16; ++e) plv[e] = clv[e];
+  };
+  // settle the pending chains
+  auto settle = [&]() __attribute__((always_inline)) {
 #pragma unroll
-                for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e)
-                  ts += __builtin_amdgcn_exp2f(pacc[e] * cl2e - pl[e]);
-              }
-              cs[j > 0 ? j - 1 : NKT - 1] += ts;
-              interleave_mfma_valu<NS, 48 / NS>();
-            } else {
+    for (int c = NKT - DIST; c < NKT; ++c) {
+      float ts[2] = {0.f, 0.f};
+      terms(c, 0, 16, plv, ts);
+      cs[c] += ts[0] + ts[1];
+    }
 #pragma unroll
-              for (int s = 0; s < NS; ++s) acc = MM::run(av[s], kf[j][s], acc);
-            }
-            pacc = acc;
-          }
+    for (int e = 0; e < 16; ++e) plv[e] = INFINITY;
+  };
+  // a sub-tile in slot U some rows of which see only part of the wave's
+  // keys: settle what is pending, then MFMAs and masked terms, unpipelined
+  auto sub_masked = [&](const QTile2<ROWB> &cur, auto u_tag) __attribute__((always_inline)) {
+    constexpr int U = decltype(u_tag)::value;
+    settle();
+    frag av[NS];
 #pragma unroll
-          for (int e = 0; e < 16; ++e) plv[e] = lv[e];
-          pend = true;
-        } else {
-          // some rows see only part of the wave's keys: masked, not pipelined
-          if (pend) {
-            cs[NKT - 1] += exp_sum(pacc, plv);
-            pend = false;
-          }
-          int qp[16];
+    for (int s = 0; s < NS; ++s) av[s] = load_frag<frag>(cur.q + swz_off<T, D>(U * 32 + col, s * 2 * E + hi * E));
 #pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4) {
-            const int4 v = *reinterpret_cast<const int4 *>(&cur.pos[sub * 32 + hi * 4 + 8 * e4]);
-            qp[4 * e4 + 0] = v.x;
-            qp[4 * e4 + 1] = v.y;
-            qp[4 * e4 + 2] = v.z;
-            qp[4 * e4 + 3] = v.w;
-          }
+    for (int j = 0; j < NKT; ++j) {
+      acc[j] = f32x16{};
 #pragma unroll
-          for (int j = 0; j < NKT; ++j) {
-            f32x16 acc = f32x16{};
+      for (int s = 0; s < NS; ++s) acc[j] = MM::run(av[s], kf[j][s], acc[j]);
+    }
 #pragma unroll
-            for (int s = 0; s < NS; ++s) acc = MM::run(av[s], kf[j][s], acc);
-            float ts = 0.f;
+    for (int e4 = 0; e4 < 4; ++e4) {
+      const int ro = U * 32 + hi * 4 + 8 * e4;
+      const float4 lv = *reinterpret_cast<const float4 *>(&cur.lse[ro]);
+      const int4 qp = *reinterpret_cast<const int4 *>(&cur.pos[ro]);
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const float x = __builtin_amdgcn_exp2f(acc[e] * cl2e - lv[e]);
-              ts += kpos[j] <= qp[e] ? x : 0.f;
-            }
-            cs[j] += ts;
-          }
-        }
+      for (int j = 0; j < NKT; ++j) {
+        const f32x16 &x = acc[j];
+        const int kp = kpos(j);
+        float t = kp <= qp.x ? __builtin_amdgcn_exp2f(x[4 * e4 + 0] * cl2e - lv.x * kLog2e) : 0.f;
+        t += kp <= qp.y ? __builtin_amdgcn_exp2f(x[4 * e4 + 1] * cl2e - lv.y * kLog2e) : 0.f;
+        t += kp <= qp.z ? __builtin_amdgcn_exp2f(x[4 * e4 + 2] * cl2e - lv.z * kLog2e) : 0.f;
+        t += kp <= qp.w ? __builtin_amdgcn_exp2f(x[4 * e4 + 3] * cl2e - lv.w * kLog2e) : 0.f;
+        cs[j] += t;
       }
     }
-    if (st + 1 < nstage) store_meta(nxt);
+  };
+
+  const int nstage = (r_hi - r_lo + QR - 1) / QR;
+  if (nstage > 0) issue_stage(r_lo, qtA);
+  auto step = [&](QTile2<ROWB> &cur, QTile2<ROWB> &nxt, int st) __attribute__((always_inline)) {
+    const int rs = r_lo + st * QR;
+    wait_vmem();
+    __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
+    if (st + 1 < nstage) issue_stage(rs + QR, nxt);
+    if (active) {
+      auto one = [&](auto u_tag) __attribute__((always_inline)) {
+        constexpr int U = decltype(u_tag)::value;
+        const int r0 = rs + U * 32;
+        const int nv = min(32, r_hi - r0);  // valid rows of the sub-tile
+        int qmin = 0x7fffffff, qmax = -1;
+        if (nv > 0) {
+          if (r0 / Tb == (r0 + nv - 1) / Tb) {  // one head: positions ascend
+            qmin = cur.pos[U * 32];
+            qmax = cur.pos[U * 32 + nv - 1];
+          } else {  // crosses a head boundary: classify as seen in part
+            qmin = -1;
+            qmax = 0x7ffffffe;
+          }
+        }
+        if (qmax >= kmin) {  // else no row of the sub-tile sees a key of the wave
+          if (qmin >= kmax) sub_tile(cur, u_tag);
+          else sub_masked(cur, u_tag);
+        }
+      };
+      one(std::integral_constant<int, 0>{});
+      one(std::integral_constant<int, 1>{});
+      one(std::integral_constant<int, 2>{});
+      one(std::integral_constant<int, 3>{});
+    }
   };
   for (int st = 0; st < nstage; st += 2) {
-    step(stA, stB, st);
-    if (st + 1 < nstage) step(stB, stA, st + 1);
+    step(qtA, qtB, st);
+    if (st + 1 < nstage) step(qtB, qtA, st + 1);
   }
   if (!active) return;
-  if (pend) cs[NKT - 1] += exp_sum(pacc, plv);
+  settle();  // the chains still pending
 #pragma unroll
   for (int j = 0; j < NKT; ++j) {
     const float v = cs[j] + __shfl_xor(cs[j], 32);
     const int key = kw0 + j * 32 + col;
-    if (hi == 0 && key < L) a.colsum[(size_t)g * a.N_tok + s0 + key] = v;
+    if (hi == 0 && key < L) a.colsum[((size_t)qsp * a.Hkv + g) * a.N_tok + s0 + key] = v;
   }
 }
 
@@ -776,7 +832,7 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
 // the per-image sum in a fixed reduction order.  Extra blocks write +inf at
 // the text positions.
 __global__ __launch_bounds__(256) void finalize_kernel(
-    const float *__restrict__ colsum, int Hq, int Hkv, int N_tok, int n_img, int T_tot,
+    const float *__restrict__ colsum, int Hq, int planes, int N_tok, int n_img, int T_tot,
     const int32_t *__restrict__ img_start, const int32_t *__restrict__ img_len,
     const int32_t *__restrict__ cu_img, const int32_t *__restrict__ cu_text,
     const int32_t *__restrict__ text_pos, int B, float *__restrict__ scores,
@@ -811,7 +867,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     float s;
     if (colsum) {
       float v = 0.f;
-      for (int g = 0; g < Hkv; ++g) v += colsum[(size_t)g * N_tok + s0 + j];
+      for (int g = 0; g < planes; ++g) v += colsum[(size_t)g * N_tok + s0 + j];
       s = nT > 0 ? v / (float)((long long)Hq * nT) : 0.f;
       scores[s0 + j] = s;
     } else {
@@ -882,10 +938,11 @@ hipError_t run_colsum(hipStream_t st, const DevLayout &L, const AttnPlan &P, con
   a.T_tot = L.T_tot;
   a.N_tok = L.N_tok;
   a.nkb = P.nkb;
+  a.nqs = P.nqs;
   a.cl2e = scale * kLog2e;
   a.colsum = (float *)(ws + P.off_colsum);
   const int nunits = L.B * Hkv;
-  const int grid = ((nunits + 7) / 8) * 8 * P.nkb;
+  const int grid = ((nunits + 7) / 8) * 8 * P.nkb * P.nqs;
   hipLaunchKernelGGL((colsum_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
@@ -915,6 +972,17 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   if (P.nkc < 1) P.nkc = 1;
   P.nkb = (L.max_seqlen + keys_per_block - 1) / keys_per_block;
   if (P.nkb < 1) P.nkb = 1;
+  // Split the query rows of pass 2 only when its grid would not fill the
+  // chip twice over (512 blocks): a block pays for loading its keys and for
+  // filling its pipeline, so fewer, longer blocks are faster; keep at least
+  // 512 rows (four stages) per split.
+  {
+    const long long base2 = (long long)L.B * Hkv * P.nkb;
+    long long nq = base2 >= 512 ? 1 : (512 + base2 - 1) / base2;
+    const long long cap = (P.rows_max + 511) / 512;
+    if (nq > cap) nq = cap;
+    P.nqs = nq < 1 ? 1 : (int)nq;
+  }
   const size_t rows = (size_t)Hq * L.T_tot;
   size_t off = 0;
   P.off_part_m = off;
@@ -924,7 +992,7 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   P.off_lse = off;
   off = align256(off + sizeof(float) * rows);
   P.off_colsum = off;
-  off = align256(off + sizeof(float) * (size_t)Hkv * L.N_tok);
+  off = align256(off + sizeof(float) * (size_t)P.nqs * Hkv * L.N_tok);
   P.bytes = off;
   return P;
 }
@@ -950,11 +1018,11 @@ hipError_t launch_colsum(hipStream_t st, const DevLayout &L, const AttnPlan &P, 
 }
 
 hipError_t launch_finalize(hipStream_t st, const DevLayout &L, const float *colsum, int Hq,
-                           int Hkv, float *scores, float *img_sum, int32_t *status) {
+                           int planes, float *scores, float *img_sum, int32_t *status) {
   const int text_blocks = (L.T_tot + 255) / 256;
   const int grid = L.n_img + text_blocks;
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL(finalize_kernel, dim3(grid), dim3(256), 0, st, colsum, Hq, Hkv, L.N_tok,
+  hipLaunchKernelGGL(finalize_kernel, dim3(grid), dim3(256), 0, st, colsum, Hq, planes, L.N_tok,
                      L.n_img, L.T_tot, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
                      L.B, scores, img_sum, status);
   return hipGetLastError();
