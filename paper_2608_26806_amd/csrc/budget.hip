@@ -1,5 +1,6 @@
 // Per-image keep budgets (Sec. 3.3.3 adaptive keep ratio, with the 5 % / 95 %
-// clamp of the appendix on alpha).  One 64-thread block per sequence.
+// clamp of the appendix on alpha).  One block per sequence, one thread per
+// image.
 //
 // The only floating-point step is the integer weight of every image,
 //   W_i = max(1, rint(min(w_i, 64) * 2^28)),
@@ -9,8 +10,8 @@
 //   * the real quota q_i = clamp(lam W_i, lo_i, hi_i) with sum q_i = K lies on
 //     the segment between two consecutive breakpoints lo_i/W_i, hi_i/W_i of
 //     f(lam) = sum_i clamp(lam W_i, lo_i, hi_i); every thread evaluates f at
-//     its breakpoints by cross-multiplication (u64), the block picks the last
-//     breakpoint with f < K and the first with f >= K;
+//     its breakpoints by cross-multiplication (u64), block reductions pick the
+//     last breakpoint with f < K and the first with f >= K;
 //   * on that segment lam = P/Q with P = K - (pinned bounds) and Q = (free
 //     weights), so q_i = P W_i / Q for free images;
 //   * largest remainder: floor(q_i), then +1 for the K - sum floor images with
@@ -60,174 +61,185 @@ __device__ double image_weight(int n, long long M, float s32, double S, bool goo
   return w;
 }
 
-__global__ __launch_bounds__(64) void budget_kernel(const float *__restrict__ img_sum,
-                                                    const int32_t *__restrict__ img_len,
-                                                    const int32_t *__restrict__ cu_img,
-                                                    const int32_t *__restrict__ keep_total,
-                                                    int mode, float alpha, int lo_pm, int hi_pm,
-                                                    int floor_abs, int32_t *__restrict__ budget,
-                                                    int32_t *__restrict__ status) {
-  __shared__ uint64_t W[kMaxImg];
-  __shared__ int32_t lo[kMaxImg], hi[kMaxImg], kk[kMaxImg];
-  __shared__ uint64_t rem[kMaxImg];
-  __shared__ uint64_t nx_num[64], nx_den[64], pv_num[64], pv_den[64];
-  __shared__ int nx_ok[64], pv_ok[64];
+constexpr int kThreads = 256;  // one thread per image (kMaxImg)
+static_assert(kMaxImg <= kThreads, "one thread per image");
+
+// Block-wide sums: wave butterflies, then the four wave partials in LDS.
+template <typename T>
+__device__ inline T block_sum(T v, T *sh) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  const T r = sh[0] + sh[1] + sh[2] + sh[3];
+  __syncthreads();  // sh may be reused right away
+  return r;
+}
+
+// Block-wide extreme of fractions num/den (den > 0) among the threads with
+// ok set: the smallest (MIN) or the largest.  Returns ok = false if none.
+template <bool MIN>
+__device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, uint64_t *shn,
+                                      uint64_t *shd, int *sho) {
+  auto better = [](uint64_t an, uint64_t ad, uint64_t bn, uint64_t bd) {
+    return MIN ? frac_lt(an, ad, bn, bd) : frac_lt(bn, bd, an, ad);
+  };
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t on = __shfl_xor(num, off), od = __shfl_xor(den, off);
+    const bool oo = __shfl_xor((int)ok, off) != 0;
+    if (oo && (!ok || better(on, od, num, den))) {
+      num = on;
+      den = od;
+      ok = true;
+    }
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    shn[w] = num;
+    shd[w] = den;
+    sho[w] = ok;
+  }
+  __syncthreads();
+  ok = false;
+  for (int t = 0; t < 4; ++t) {
+    if (sho[t] && (!ok || better(shn[t], shd[t], num, den))) {
+      num = shn[t];
+      den = shd[t];
+      ok = true;
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restrict__ img_sum,
+                                                          const int32_t *__restrict__ img_len,
+                                                          const int32_t *__restrict__ cu_img,
+                                                          const int32_t *__restrict__ keep_total,
+                                                          int mode, float alpha, int lo_pm, int hi_pm,
+                                                          int floor_abs, int32_t *__restrict__ budget,
+                                                          int32_t *__restrict__ status) {
+  __shared__ uint64_t W[kMaxImg], rem[kMaxImg];
+  __shared__ int32_t lo[kMaxImg], hi[kMaxImg];
+  __shared__ float sv[kMaxImg];
+  __shared__ long long red_i[4];
+  __shared__ uint64_t red_u[4], ext_n[4], ext_d[4];
+  __shared__ int ext_o[4];
   __shared__ double sh_S;
-  __shared__ long long sh_M;
-  __shared__ uint64_t sh_P, sh_Q;
-  __shared__ int sh_bad;
 
   const int b = blockIdx.x, tid = threadIdx.x;
   const int i0 = cu_img[b], m = cu_img[b + 1] - i0;
   const long long K = keep_total[b];
   if (m <= 0) return;
+  const bool mine = tid < m;  // this thread's image is tid
 
-  for (int i = tid; i < m; i += 64) {
-    const long long n = img_len[i0 + i];
-    long long l = (lo_pm * n + 999) / 1000;
+  long long n = 0, l = 0, h = 0;
+  float s32 = 0.f;
+  if (mine) {
+    n = img_len[i0 + tid];
+    s32 = img_sum[i0 + tid];
+    l = (lo_pm * n + 999) / 1000;
     if (l < floor_abs) l = floor_abs;
     if (l > n) l = n;
-    long long h = (hi_pm * n) / 1000;
+    h = (hi_pm * n) / 1000;
     if (h < l) h = l;
-    lo[i] = (int32_t)l;
-    hi[i] = (int32_t)h;
+    lo[tid] = (int32_t)l;
+    hi[tid] = (int32_t)h;
+    sv[tid] = s32;
   }
-  if (tid == 0) {
+  const long long M = block_sum(n, red_i);
+  const long long slo = block_sum(l, red_i);
+  const long long shi = block_sum(h, red_i);
+  if (tid == 0) {  // the image sum, in image order (it fixes the weights)
     double S = 0.0;
-    long long M = 0;
-    for (int i = 0; i < m; ++i) {
-      S = S + (double)img_sum[i0 + i];
-      M += img_len[i0 + i];
-    }
+    for (int i = 0; i < m; ++i) S = S + (double)sv[i];
     sh_S = S;
-    sh_M = M;
   }
   __syncthreads();
   const double S = sh_S;
   const bool good = isfinite(S) && S > 0.0;
-  for (int i = tid; i < m; i += 64) {
-    const int n = img_len[i0 + i];
-    const double w = image_weight(n, sh_M, img_sum[i0 + i], S, good, mode, (double)alpha, (int)K);
-    uint64_t q = 0;
+  uint64_t Wi = 0;
+  if (mine) {
+    const double w = image_weight((int)n, M, s32, S, good, mode, (double)alpha, (int)K);
     if (n > 0) {
-      q = (uint64_t)rint(w * (double)(1ll << kWeightBits));
-      if (q < 1) q = 1;
+      Wi = (uint64_t)rint(w * (double)(1ll << kWeightBits));
+      if (Wi < 1) Wi = 1;
     }
-    W[i] = q;
+    W[tid] = Wi;
   }
-  if (tid == 0) {
-    long long slo = 0, shi = 0;
-    for (int i = 0; i < m; ++i) {
-      slo += lo[i];
-      shi += hi[i];
-    }
-    sh_bad = (K < slo || K > shi) ? 1 : 0;
-  }
-  __syncthreads();
-  if (sh_bad) {  // the host checks this too; keep outputs defined anyway
-    for (int i = tid; i < m; i += 64) budget[i0 + i] = lo[i];
+  if (K < slo || K > shi) {  // the host checks this too; keep outputs defined anyway
+    if (mine) budget[i0 + tid] = (int32_t)l;
     if (tid == 0 && status) atomicOr(status + b, AVTP_FLAG_INFEASIBLE);
     return;
   }
+  __syncthreads();
 
-  // breakpoints k < m: lo_k / W_k ; k >= m: hi_(k-m) / W_(k-m); zero-length images have none
-  bool has_nx = false, has_pv = false;
+  // Breakpoints k < m: lo_k / W_k, k >= m: hi_(k-m) / W_(k-m) (zero-length
+  // images have none).  Each thread evaluates f at its breakpoints and keeps
+  // the smallest with f >= K (next) and the largest with f < K (prev).
+  bool hn = false, hp = false;
   uint64_t bn = 0, bd = 1, pn = 0, pd = 1;
-  for (int k = tid; k < 2 * m; k += 64) {
+  for (int k = tid; k < 2 * m; k += kThreads) {
     const int i = k < m ? k : k - m;
     if (W[i] == 0) continue;
     const uint64_t num = (uint64_t)(k < m ? lo[i] : hi[i]), den = W[i];
     uint64_t f = 0;  // f(num/den) * den
     for (int j = 0; j < m; ++j) {
-      if (W[j] == 0) continue;
-      uint64_t v = num * W[j];
-      const uint64_t l = (uint64_t)lo[j] * den, h = (uint64_t)hi[j] * den;
-      v = v < l ? l : (v > h ? h : v);
+      const uint64_t wj = W[j];
+      if (wj == 0) continue;
+      uint64_t v = num * wj;
+      const uint64_t lj = (uint64_t)lo[j] * den, hj = (uint64_t)hi[j] * den;
+      v = v < lj ? lj : (v > hj ? hj : v);
       f += v;
     }
     if (f >= (uint64_t)K * den) {
-      if (!has_nx || frac_lt(num, den, bn, bd)) {
+      if (!hn || frac_lt(num, den, bn, bd)) {
         bn = num;
         bd = den;
-        has_nx = true;
-      }
-    } else {
-      if (!has_pv || frac_lt(pn, pd, num, den)) {
-        pn = num;
-        pd = den;
-        has_pv = true;
-      }
-    }
-  }
-  nx_num[tid] = bn;
-  nx_den[tid] = bd;
-  nx_ok[tid] = has_nx;
-  pv_num[tid] = pn;
-  pv_den[tid] = pd;
-  pv_ok[tid] = has_pv;
-  __syncthreads();
-  if (tid == 0) {
-    bool hn = false, hp = false;
-    for (int t = 0; t < 64; ++t) {
-      if (nx_ok[t] && (!hn || frac_lt(nx_num[t], nx_den[t], bn, bd))) {
-        bn = nx_num[t];
-        bd = nx_den[t];
         hn = true;
       }
-      if (pv_ok[t] && (!hp || frac_lt(pn, pd, pv_num[t], pv_den[t]))) {
-        pn = pv_num[t];
-        pd = pv_den[t];
-        hp = true;
-      }
-    }
-    // classify images on the open segment (prev, next]
-    uint64_t pinned = 0, Q = 0;
-    for (int i = 0; i < m; ++i) {
-      if (W[i] == 0) {
-        kk[i] = 0;
-        rem[i] = 0;
-        continue;
-      }
-      const bool low = hn && !frac_lt((uint64_t)lo[i], W[i], bn, bd);       // lo/W >= next
-      const bool high = hp && !frac_lt(pn, pd, (uint64_t)hi[i], W[i]);      // hi/W <= prev
-      if (low || (!hn)) {
-        kk[i] = lo[i];
-        rem[i] = 0;
-        pinned += lo[i];
-      } else if (high) {
-        kk[i] = hi[i];
-        rem[i] = 0;
-        pinned += hi[i];
-      } else {
-        kk[i] = -1;  // free
-        Q += W[i];
-      }
-    }
-    sh_P = (uint64_t)K - pinned;
-    sh_Q = Q;
-  }
-  __syncthreads();
-  const uint64_t P = sh_P, Q = sh_Q;
-  for (int i = tid; i < m; i += 64) {
-    if (kk[i] == -1) {
-      const uint64_t num = P * W[i];
-      kk[i] = (int32_t)(num / Q);
-      rem[i] = num % Q;
+    } else if (!hp || frac_lt(pn, pd, num, den)) {
+      pn = num;
+      pd = den;
+      hp = true;
     }
   }
-  __syncthreads();
-  __shared__ long long sh_D;
-  if (tid == 0) {
-    long long s = 0;
-    for (int i = 0; i < m; ++i) s += kk[i];
-    sh_D = K - s;
+  block_frac_ext<true>(bn, bd, hn, ext_n, ext_d, ext_o);
+  block_frac_ext<false>(pn, pd, hp, ext_n, ext_d, ext_o);
+
+  // classify the images on the segment (prev, next]: pinned at lo, at hi, or free
+  int32_t kk = 0;
+  uint64_t pinned = 0, freeW = 0;
+  bool fr = false;
+  if (mine && Wi != 0) {
+    const bool low = hn && !frac_lt((uint64_t)l, Wi, bn, bd);   // lo/W >= next
+    const bool high = hp && !frac_lt(pn, pd, (uint64_t)h, Wi);  // hi/W <= prev
+    if (low || !hn) {
+      kk = (int32_t)l;
+      pinned = (uint64_t)l;
+    } else if (high) {
+      kk = (int32_t)h;
+      pinned = (uint64_t)h;
+    } else {
+      fr = true;
+      freeW = Wi;
+    }
   }
-  __syncthreads();
-  const long long D = sh_D;
-  for (int i = tid; i < m; i += 64) {
+  const uint64_t P = (uint64_t)K - block_sum(pinned, red_u);
+  const uint64_t Q = block_sum(freeW, red_u);
+  uint64_t ri = 0;
+  if (fr) {
+    const uint64_t num = P * Wi;
+    kk = (int32_t)(num / Q);
+    ri = num % Q;
+  }
+  if (mine) rem[tid] = ri;
+  const long long D = K - block_sum((long long)kk, red_i);  // the units left to hand out
+  // largest remainders first, lowest image index among equal ones
+  if (mine) {
     long long rank = 0;
-    for (int j = 0; j < m; ++j) rank += (rem[j] > rem[i]) || (rem[j] == rem[i] && j < i);
-    budget[i0 + i] = kk[i] + (rank < D ? 1 : 0);
+    for (int j = 0; j < m; ++j) rank += (rem[j] > ri) || (rem[j] == ri && j < tid);
+    budget[i0 + tid] = kk + (rank < D ? 1 : 0);
   }
 }
 
@@ -236,7 +248,7 @@ __global__ __launch_bounds__(64) void budget_kernel(const float *__restrict__ im
 hipError_t launch_budget(hipStream_t st, const DevLayout &L, const float *img_sum, int mode,
                          float alpha, int lo_permille, int hi_permille, int floor_abs,
                          int32_t *budget, int32_t *status) {
-  hipLaunchKernelGGL(budget_kernel, dim3(L.B), dim3(64), 0, st, img_sum, L.img_len, L.cu_img,
+  hipLaunchKernelGGL(budget_kernel, dim3(L.B), dim3(kThreads), 0, st, img_sum, L.img_len, L.cu_img,
                      L.keep_total, mode, alpha, lo_permille, hi_permille, floor_abs, budget,
                      status);
   return hipGetLastError();

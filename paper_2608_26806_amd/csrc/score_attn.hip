@@ -269,12 +269,22 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   const int R = a.G * Tb;
   const int row0 = qb * QB;
   const int kbeg = kc * a.kchunk;
-  if (row0 >= R || kbeg >= L) return;
-  const int kend = min(L, kbeg + a.kchunk);
+  if (row0 >= R) return;
+  const size_t HqT = (size_t)a.Hq * a.T_tot;
   const int32_t *tp = a.text_pos + t0;
-  int bmin, bmax;
-  rows_pos_range(tp, Tb, row0, min(R, row0 + QB), bmin, bmax);
-  if (s0 + kbeg > bmax) return;                  // chunk starts after every row of the block
+  int bmin = 0, bmax = -1;
+  if (kbeg < L) rows_pos_range(tp, Tb, row0, min(R, row0 + QB), bmin, bmax);
+  if (kbeg >= L || s0 + kbeg > bmax) {
+    // no row of the block sees a key of the chunk: empty partials, so that
+    // the combine can read every chunk of every row
+    for (int r = row0 + (int)threadIdx.x; r < min(R, row0 + QB); r += kThreads) {
+      const int hh = r / Tb, qidx = (g * a.G + hh) * a.T_tot + t0 + (r - hh * Tb);
+      a.part_m[kc * HqT + qidx] = -INFINITY;
+      a.part_l[kc * HqT + qidx] = 0.f;
+    }
+    return;
+  }
+  const int kend = min(L, kbeg + a.kchunk);
   const int kstop = min(kend, bmax - s0 + 1);    // keys after the last row are never visible
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -486,7 +496,6 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   if (ntw > 0 && ntw % TPS == 0) tile(smA, 0, P0{}, std::true_type{}, std::false_type{});
 
   // merge the two half-waves (same query column, disjoint keys) and store
-  const size_t HqT = (size_t)a.Hq * a.T_tot;
 #pragma unroll
   for (int i = 0; i < NT; ++i) {
     const float om = __shfl_xor(ref[i], 32), ol = __shfl_xor(l[i], 32);
@@ -505,29 +514,18 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
 }
 
 // Merge the chunk partials of every text row into lse = ln(sum exp(z)).
-// Only the chunks that start at or before the row's position hold keys it
-// can see, and exactly those were written by pass 1.
+// Pass 1 writes a partial for every (chunk, row), empty (-inf, 0) where the
+// row sees no key of the chunk.
 __global__ void lse_combine_kernel(const float *__restrict__ part_m, const float *__restrict__ part_l,
-                                   const int32_t *__restrict__ cu_seqlens,
-                                   const int32_t *__restrict__ cu_text,
-                                   const int32_t *__restrict__ text_pos, int B, int Hq, int T_tot,
-                                   int kchunk, float *__restrict__ lse) {
+                                   int rows, int nkc, float *__restrict__ lse) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= Hq * T_tot) return;
-  const int t = idx % T_tot;
-  int lo = 0, hi = B - 1;  // sequence of text row t
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (cu_text[mid] <= t) lo = mid; else hi = mid - 1;
-  }
-  const int last = (text_pos[t] - cu_seqlens[lo]) / kchunk;
-  const size_t HqT = (size_t)Hq * T_tot;
+  if (idx >= rows) return;
   float M = -INFINITY;
-  for (int c = 0; c <= last; ++c) M = fmaxf(M, part_m[c * HqT + idx]);
+  for (int c = 0; c < nkc; ++c) M = fmaxf(M, part_m[(size_t)c * rows + idx]);
   float S = 0.f;
-  for (int c = 0; c <= last; ++c) {
-    const float m = part_m[c * HqT + idx];
-    if (m != -INFINITY) S += part_l[c * HqT + idx] * __builtin_amdgcn_exp2f(m - M);
+  for (int c = 0; c < nkc; ++c) {
+    const float m = part_m[(size_t)c * rows + idx];
+    if (m != -INFINITY) S += part_l[(size_t)c * rows + idx] * __builtin_amdgcn_exp2f(m - M);
   }
   lse[idx] = (M + __builtin_amdgcn_logf(S)) * kLn2;
 }
@@ -838,6 +836,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     const int32_t *__restrict__ text_pos, int B, float *__restrict__ scores,
     float *__restrict__ img_sum, int32_t *__restrict__ status) {
   __shared__ float red[256];
+  __shared__ int sh_b, sh_cnt[4];
   const int tid = threadIdx.x;
   if ((int)blockIdx.x >= n_img) {
     const int t = (blockIdx.x - n_img) * 256 + tid;
@@ -845,21 +844,20 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     return;
   }
   const int i = blockIdx.x;
-  int lo = 0, hi = B - 1;  // sequence of image i
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (cu_img[mid] <= i) lo = mid; else hi = mid - 1;
-  }
-  const int b = lo;
+  for (int c = tid; c < B; c += 256)  // the sequence holding image i
+    if (cu_img[c] <= i && i < cu_img[c + 1]) sh_b = c;
+  __syncthreads();
+  const int b = sh_b;
   const int s0 = img_start[i], n = img_len[i];
   int nT = 0;
-  if (colsum) {  // text rows after the image: those past the first one beyond s0
-    int a0 = cu_text[b], a1 = cu_text[b + 1];
-    while (a0 < a1) {
-      const int mid = (a0 + a1) >> 1;
-      if (text_pos[mid] < s0) a0 = mid + 1; else a1 = mid;
-    }
-    nT = cu_text[b + 1] - a0;
+  if (colsum) {  // text rows after the image (their positions exceed s0)
+    int c = 0;
+    for (int t = cu_text[b] + tid; t < cu_text[b + 1]; t += 256) c += text_pos[t] > s0;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+    if ((tid & 63) == 0) sh_cnt[tid >> 6] = c;
+    __syncthreads();
+    nT = sh_cnt[0] + sh_cnt[1] + sh_cnt[2] + sh_cnt[3];
   }
   float acc = 0.f;
   bool nan = false;
@@ -916,8 +914,7 @@ hipError_t run_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P, co
   if (e != hipSuccess) return e;
   const int rows = Hq * L.T_tot;
   hipLaunchKernelGGL(lse_combine_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, a.part_m,
-                     a.part_l, L.cu_seqlens, L.cu_text, L.text_pos, L.B, Hq, L.T_tot, P.kchunk,
-                     row_lse);
+                     a.part_l, rows, P.nkc, row_lse);
   return hipGetLastError();
 }
 

@@ -172,14 +172,19 @@ def test_budget_at_bounds(K_at):
 
 
 # ------------------------------------------------------------------ select
-def _sel_layout():
-    return build_layout([[37, 1, 0, 300], [5, 64], [1000]], 3, 5, 40)
+def _sel_layout(kind):
+    if kind == "mixed":
+        return build_layout([[37, 1, 0, 300], [5, 64], [1000]], 3, 5, 40)
+    # sequences without images (first, middle, last), images with no text
+    # before them, and one image longer than the kernel keeps in LDS
+    return build_layout([[], [9000, 3], [], [50, 0, 7], []], 0, 6, 40)
 
 
+@pytest.mark.parametrize("kind", ["mixed", "gaps"])
 @pytest.mark.parametrize("pattern", ["random", "ties", "specials"])
-def test_select_bit_exact(pattern):
-    lay = _sel_layout()
-    rng = np.random.default_rng(len(pattern))
+def test_select_bit_exact(pattern, kind):
+    lay = _sel_layout(kind)
+    rng = np.random.default_rng(len(pattern) + 10 * len(kind))
     s = np.full(lay.N_tok, np.inf, np.float32)
     for i in range(lay.n_img):
         st, n = int(lay.img_start[i]), int(lay.img_len[i])
@@ -195,7 +200,7 @@ def test_select_bit_exact(pattern):
     dl = A.DeviceLayout({**{nm: getattr(lay, nm) for nm in A.DeviceLayout.NAMES},
                          "keep_total": [int(budgets[lay.cu_img[b]:lay.cu_img[b + 1]].sum())
                                         for b in range(lay.B)]})
-    say(f"[select] pattern={pattern}")
+    say(f"[select] pattern={pattern} layout={kind}")
     keep, cu = A.select(dl, torch.from_numpy(s).cuda(), torch.from_numpy(budgets).cuda())
     keep_o, cu_o = O.select(lay, s, budgets)
     assert np.array_equal(keep.cpu().numpy(), keep_o)
