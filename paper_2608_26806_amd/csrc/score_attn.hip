@@ -463,11 +463,13 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
         else tile(buf, KT * 32, par_tag{}, std::true_type{}, std::true_type{});
         pend_kb = ks + KT * 32;
       };
-      static_assert(TPS == 4, "one stage is four key tiles");
+      static_assert(TPS == 2 || TPS == 4, "one stage is two or four key tiles");
       one(std::integral_constant<int, 0>{});
       one(std::integral_constant<int, 1>{});
-      one(std::integral_constant<int, 2>{});
-      one(std::integral_constant<int, 3>{});
+      if constexpr (TPS == 4) {
+        one(std::integral_constant<int, 2>{});
+        one(std::integral_constant<int, 3>{});
+      }
     } else if (st * TPS < ntw) {
       // the wave's last tiles, then settle the pending one (masked variant)
       auto one = [&](auto kt_tag) __attribute__((always_inline)) {
@@ -483,8 +485,10 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
       };
       one(std::integral_constant<int, 0>{});
       one(std::integral_constant<int, 1>{});
-      one(std::integral_constant<int, 2>{});
-      one(std::integral_constant<int, 3>{});
+      if constexpr (TPS == 4) {
+        one(std::integral_constant<int, 2>{});
+        one(std::integral_constant<int, 3>{});
+      }
     }
   };
   for (int st = 0; st < nstage; st += 2) {
@@ -635,16 +639,16 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   const float *lbase = a.lse + (size_t)g * a.G * a.T_tot + t0;     // head g*G, text row 0
   using DP = DmaPlan<T, D, QR>;
   // One stage: query rows, their LSE and positions.  Wave 0 loads the LSE,
-  // wave 1 the positions, 64 rows per instruction.
-  auto issue_stage = [&](int rs, QTile2<ROWB> &dst) __attribute__((always_inline)) {
-    const int hh = rs / Tb;
-    const bool one_head = rs + QR <= r_hi && (rs + QR - 1) / Tb == hh;
+  // wave 1 the positions, 64 rows per instruction.  (hh, toff): head and
+  // text row of the stage's first row rs.
+  auto issue_stage = [&](int rs, int hh, int toff, QTile2<ROWB> &dst) __attribute__((always_inline)) {
+    const bool one_head = rs + QR <= r_hi && toff + QR <= Tb;
     if (one_head) {  // consecutive text rows of one head
       int ln = lane;
       asm volatile("" : "+v"(ln));
       uint32_t dlo[DP::PER];
       DP::lane_offsets(dlo, ln, qstride);
-      DP::issue(dst.q, qbase + ((size_t)(rs - hh * Tb) * a.Hq + hh) * ROWB, wave, dlo, qstride);
+      DP::issue(dst.q, qbase + ((size_t)toff * a.Hq + hh) * ROWB, wave, dlo, qstride);
     } else {
       dma_stage<T, D, QR>(dst.q, qbase, wave, lane, [&](int row) __attribute__((always_inline)) {
         const int r = min(rs + row, R - 1);  // rows past R re-read row R-1; their lse is +inf
@@ -655,21 +659,31 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
     if (wave < 2) {
 #pragma unroll
       for (int i = 0; i < QR / 64; ++i) {
-        const int r = rs + i * 64 + lane;
         const void *src;
         if (one_head) {
-          const int t = r - hh * Tb;
+          const int t = toff + i * 64 + lane;
           src = wave == 0 ? (const void *)(lbase + (size_t)hh * a.T_tot + t) : (const void *)(tp + t);
-        } else if (r < r_hi) {
-          const int h2 = r / Tb, t = r - h2 * Tb;
-          src = wave == 0 ? (const void *)(lbase + (size_t)h2 * a.T_tot + t) : (const void *)(tp + t);
         } else {
-          src = wave == 0 ? (const void *)&kRowNone : (const void *)&kPosNone;
+          const int r = rs + i * 64 + lane;
+          if (r < r_hi) {
+            const int h2 = r / Tb, t = r - h2 * Tb;
+            src = wave == 0 ? (const void *)(lbase + (size_t)h2 * a.T_tot + t) : (const void *)(tp + t);
+          } else {
+            src = wave == 0 ? (const void *)&kRowNone : (const void *)&kPosNone;
+          }
         }
         void *dstp = wave == 0 ? (void *)(dst.lse + i * 64) : (void *)(dst.pos + i * 64);
         __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
                                          (__attribute__((address_space(3))) void *)dstp, 4, 0, 0);
       }
+    }
+  };
+  // the text row index of the row QR rows further, and its head
+  auto advance = [&](int &hh, int &toff) __attribute__((always_inline)) {
+    toff += QR;
+    while (toff >= Tb) {
+      toff -= Tb;
+      ++hh;
     }
   };
 
@@ -779,20 +793,25 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   };
 
   const int nstage = (r_hi - r_lo + QR - 1) / QR;
-  if (nstage > 0) issue_stage(r_lo, qtA);
+  int ch = r_lo / Tb, ct = r_lo - ch * Tb;  // head and text row of the current stage's first row
+  if (nstage > 0) issue_stage(r_lo, ch, ct, qtA);
   auto step = [&](QTile2<ROWB> &cur, QTile2<ROWB> &nxt, int st) __attribute__((always_inline)) {
     const int rs = r_lo + st * QR;
+    int nh = ch, nt = ct;
+    advance(nh, nt);
     wait_vmem();
     __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
-    if (st + 1 < nstage) issue_stage(rs + QR, nxt);
+    if (st + 1 < nstage) issue_stage(rs + QR, nh, nt, nxt);
     if (active) {
       auto one = [&](auto u_tag) __attribute__((always_inline)) {
         constexpr int U = decltype(u_tag)::value;
         const int r0 = rs + U * 32;
         const int nv = min(32, r_hi - r0);  // valid rows of the sub-tile
+        int tt = ct + U * 32;               // its first text row, within its head
+        while (tt >= Tb) tt -= Tb;
         int qmin = 0x7fffffff, qmax = -1;
         if (nv > 0) {
-          if (r0 / Tb == (r0 + nv - 1) / Tb) {  // one head: positions ascend
+          if (tt + nv <= Tb) {  // one head: positions ascend
             qmin = cur.pos[U * 32];
             qmax = cur.pos[U * 32 + nv - 1];
           } else {  // crosses a head boundary: classify as seen in part
@@ -810,6 +829,8 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
       one(std::integral_constant<int, 2>{});
       one(std::integral_constant<int, 3>{});
     }
+    ch = nh;
+    ct = nt;
   };
   for (int st = 0; st < nstage; st += 2) {
     step(qtA, qtB, st);
