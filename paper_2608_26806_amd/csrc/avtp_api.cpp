@@ -126,7 +126,7 @@ int avtp_row_lse(avtp_stream_t stream, const avtp_layout *layout, int dtype, con
   if (!ws || ws_bytes < P.bytes || (uintptr_t)ws % 256) return AVTP_ERR_WORKSPACE;
   if (L.T_tot == 0) return AVTP_OK;
   return hip_status(launch_row_lse((hipStream_t)stream, L, P, dtype, q_text, k, Hq, Hkv, d,
-                                   softmax_scale, row_lse_out, (char *)ws));
+                                   softmax_scale, row_lse_out, nullptr, (char *)ws));
 }
 
 int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dtype,
@@ -158,15 +158,16 @@ int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
   if (!ws || ws_bytes < P.bytes || (uintptr_t)ws % 256) return AVTP_ERR_WORKSPACE;
   char *w = (char *)ws;
   hipError_t e = hipSuccess;
-  const float *lse = row_lse;
-  if (!lse) {
-    float *own = (float *)(w + P.off_lse);
-    if (L.T_tot > 0)
-      e = launch_row_lse(st, L, P, dtype, q_text, k, Hq, Hkv, d, softmax_scale, own, w);
-    lse = own;
+  float *lse2 = (float *)(w + P.off_lse2);  // row LSE in log2 units, for pass 2
+  if (L.T_tot > 0) {
+    if (row_lse)
+      e = launch_lse_to_log2(st, Hq * L.T_tot, row_lse, lse2);
+    else
+      e = launch_row_lse(st, L, P, dtype, q_text, k, Hq, Hkv, d, softmax_scale,
+                         (float *)(w + P.off_lse), lse2, w);
   }
   if (e == hipSuccess && L.T_tot > 0)
-    e = launch_colsum(st, L, P, dtype, q_text, k, Hq, Hkv, d, softmax_scale, lse, w);
+    e = launch_colsum(st, L, P, dtype, q_text, k, Hq, Hkv, d, softmax_scale, lse2, w);
   if (e == hipSuccess)
     e = launch_finalize(st, L, (const float *)(w + P.off_colsum), Hq, Hkv * P.nqs, scores, img_sum,
                         status);

@@ -28,18 +28,23 @@ struct AttnPlan {
   int nkc;        // chunks per sequence (max)
   int nkb;        // key blocks per (sequence, key head) in pass 2
   int nqs;        // query splits of pass 2 (column-sum planes per key head)
-  size_t off_part_m, off_part_l, off_lse, off_colsum, bytes;
+  size_t off_part_m, off_part_l, off_lse, off_lse2, off_colsum, bytes;
 };
 
 AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype);
 size_t variation_workspace_bytes(const DevLayout &L);
 
+// Pass 1 and the combine: the row LSE (natural log) into row_lse and, if
+// lse2 is not null, in log2 units into lse2.
 hipError_t launch_row_lse(hipStream_t stream, const DevLayout &L, const AttnPlan &P, int dtype,
                           const void *q, const void *k, int Hq, int Hkv, int d, float scale,
-                          float *row_lse, char *ws);
+                          float *row_lse, float *lse2, char *ws);
+// lse2 = lse * log2(e) for `rows` rows (an LSE the caller supplies)
+hipError_t launch_lse_to_log2(hipStream_t stream, int rows, const float *lse, float *lse2);
+// Pass 2: column sums from the row LSE in log2 units.
 hipError_t launch_colsum(hipStream_t stream, const DevLayout &L, const AttnPlan &P, int dtype,
                          const void *q, const void *k, int Hq, int Hkv, int d, float scale,
-                         const float *row_lse, char *ws);
+                         const float *lse2, char *ws);
 // Per-image finalisation shared by both score modes.  colsum == nullptr:
 // scores already hold the per-token values (variation mode); otherwise the
 // score of token j is the sum of `planes` column-sum planes at j over

@@ -517,11 +517,13 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   }
 }
 
-// Merge the chunk partials of every text row into lse = ln(sum exp(z)).
-// Pass 1 writes a partial for every (chunk, row), empty (-inf, 0) where the
-// row sees no key of the chunk.
+// Merge the chunk partials of every text row into lse = ln(sum exp(z)), and
+// (if lse2 is given) the same in log2 units for pass 2.  Pass 1 writes a
+// partial for every (chunk, row), empty (-inf, 0) where the row sees no key
+// of the chunk.
 __global__ void lse_combine_kernel(const float *__restrict__ part_m, const float *__restrict__ part_l,
-                                   int rows, int nkc, float *__restrict__ lse) {
+                                   int rows, int nkc, float *__restrict__ lse,
+                                   float *__restrict__ lse2) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= rows) return;
   float M = -INFINITY;
@@ -531,7 +533,16 @@ __global__ void lse_combine_kernel(const float *__restrict__ part_m, const float
     const float m = part_m[(size_t)c * rows + idx];
     if (m != -INFINITY) S += part_l[(size_t)c * rows + idx] * __builtin_amdgcn_exp2f(m - M);
   }
-  lse[idx] = (M + __builtin_amdgcn_logf(S)) * kLn2;
+  const float v = (M + __builtin_amdgcn_logf(S)) * kLn2;
+  lse[idx] = v;
+  // log2 units from the rounded natural value, exactly as for a supplied LSE
+  if (lse2) lse2[idx] = v * kLog2e;
+}
+
+// Row LSE in natural log -> log2 units (for an LSE the caller supplies).
+__global__ void lse_to_log2_kernel(const float *__restrict__ lse, int rows, float *__restrict__ lse2) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < rows) lse2[idx] = lse[idx] * kLog2e;
 }
 
 // Pass-2 LDS stage: kStage query rows (swizzled) with their row LSE and
@@ -543,13 +554,13 @@ __device__ const int kPosNone = -1;
 template <int ROWB>
 struct __attribute__((aligned(16))) QTile2 {
   char q[kStage * ROWB];
-  float lse[kStage];  // natural log
+  float lse[kStage];  // log2 units
   int pos[kStage];
 };
 
 struct P2Args {
   const char *q, *k;
-  const float *lse;
+  const float *lse2;  // row LSE in log2 units, [Hq][T_tot]
   const int32_t *cu_seqlens, *cu_text, *text_pos;
   int B, Hq, Hkv, G, T_tot, N_tok, nkb, nqs;
   float cl2e;
@@ -636,7 +647,7 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
 
   const char *qbase = a.q + ((size_t)t0 * a.Hq + g * a.G) * ROWB;  // text row 0, head g*G
   const uint32_t qstride = (uint32_t)a.Hq * ROWB;
-  const float *lbase = a.lse + (size_t)g * a.G * a.T_tot + t0;     // head g*G, text row 0
+  const float *lbase = a.lse2 + (size_t)g * a.G * a.T_tot + t0;    // head g*G, text row 0
   using DP = DmaPlan<T, D, QR>;
   // One stage: query rows, their LSE and positions.  Wave 0 loads the LSE,
   // wave 1 the positions, 64 rows per instruction.  (hh, toff): head and
@@ -703,15 +714,15 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
 #pragma unroll
     for (int e = e0; e < e1; ++e) ts[e & 1] += __builtin_amdgcn_exp2f(acc[c][e] * cl2e - lv[e]);
   };
-  // the sub-tile's LSE of this lane's rows, in log2 units
+  // the sub-tile's LSE of this lane's rows (log2 units)
   auto load_lv = [&](const QTile2<ROWB> &cur, int U, float (&lv)[16]) __attribute__((always_inline)) {
 #pragma unroll
     for (int e4 = 0; e4 < 4; ++e4) {
       const float4 x = *reinterpret_cast<const float4 *>(&cur.lse[U * 32 + hi * 4 + 8 * e4]);
-      lv[4 * e4 + 0] = x.x * kLog2e;
-      lv[4 * e4 + 1] = x.y * kLog2e;
-      lv[4 * e4 + 2] = x.z * kLog2e;
-      lv[4 * e4 + 3] = x.w * kLog2e;
+      lv[4 * e4 + 0] = x.x;
+      lv[4 * e4 + 1] = x.y;
+      lv[4 * e4 + 2] = x.z;
+      lv[4 * e4 + 3] = x.w;
     }
   };
   // a sub-tile in stage slot U that every row of which sees every key of the
@@ -783,10 +794,10 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
       for (int j = 0; j < NKT; ++j) {
         const f32x16 &x = acc[j];
         const int kp = kpos(j);
-        float t = kp <= qp.x ? __builtin_amdgcn_exp2f(x[4 * e4 + 0] * cl2e - lv.x * kLog2e) : 0.f;
-        t += kp <= qp.y ? __builtin_amdgcn_exp2f(x[4 * e4 + 1] * cl2e - lv.y * kLog2e) : 0.f;
-        t += kp <= qp.z ? __builtin_amdgcn_exp2f(x[4 * e4 + 2] * cl2e - lv.z * kLog2e) : 0.f;
-        t += kp <= qp.w ? __builtin_amdgcn_exp2f(x[4 * e4 + 3] * cl2e - lv.w * kLog2e) : 0.f;
+        float t = kp <= qp.x ? __builtin_amdgcn_exp2f(x[4 * e4 + 0] * cl2e - lv.x) : 0.f;
+        t += kp <= qp.y ? __builtin_amdgcn_exp2f(x[4 * e4 + 1] * cl2e - lv.y) : 0.f;
+        t += kp <= qp.z ? __builtin_amdgcn_exp2f(x[4 * e4 + 2] * cl2e - lv.z) : 0.f;
+        t += kp <= qp.w ? __builtin_amdgcn_exp2f(x[4 * e4 + 3] * cl2e - lv.w) : 0.f;
         cs[j] += t;
       }
     }
@@ -910,7 +921,8 @@ __global__ __launch_bounds__(256) void finalize_kernel(
 
 template <typename T, int D>
 hipError_t run_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P, const void *q,
-                       const void *k, int Hq, int Hkv, float scale, float *row_lse, char *ws) {
+                       const void *k, int Hq, int Hkv, float scale, float *row_lse, float *lse2,
+                       char *ws) {
   P1Args a;
   a.q = (const char *)q;
   a.k = (const char *)k;
@@ -935,17 +947,17 @@ hipError_t run_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P, co
   if (e != hipSuccess) return e;
   const int rows = Hq * L.T_tot;
   hipLaunchKernelGGL(lse_combine_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, a.part_m,
-                     a.part_l, rows, P.nkc, row_lse);
+                     a.part_l, rows, P.nkc, row_lse, lse2);
   return hipGetLastError();
 }
 
 template <typename T, int D>
 hipError_t run_colsum(hipStream_t st, const DevLayout &L, const AttnPlan &P, const void *q,
-                      const void *k, int Hq, int Hkv, float scale, const float *lse, char *ws) {
+                      const void *k, int Hq, int Hkv, float scale, const float *lse2, char *ws) {
   P2Args a;
   a.q = (const char *)q;
   a.k = (const char *)k;
-  a.lse = lse;
+  a.lse2 = lse2;
   a.cu_seqlens = L.cu_seqlens;
   a.cu_text = L.cu_text;
   a.text_pos = L.text_pos;
@@ -1009,6 +1021,8 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   off = align256(off + sizeof(float) * rows * P.nkc);
   P.off_lse = off;
   off = align256(off + sizeof(float) * rows);
+  P.off_lse2 = off;
+  off = align256(off + sizeof(float) * rows);
   P.off_colsum = off;
   off = align256(off + sizeof(float) * (size_t)P.nqs * Hkv * L.N_tok);
   P.bytes = off;
@@ -1017,22 +1031,28 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
 
 hipError_t launch_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P, int dtype,
                           const void *q, const void *k, int Hq, int Hkv, int d, float scale,
-                          float *row_lse, char *ws) {
+                          float *row_lse, float *lse2, char *ws) {
   if (dtype == AVTP_BF16)
-    return d == 128 ? run_row_lse<__bf16, 128>(st, L, P, q, k, Hq, Hkv, scale, row_lse, ws)
-                    : run_row_lse<__bf16, 64>(st, L, P, q, k, Hq, Hkv, scale, row_lse, ws);
-  return d == 128 ? run_row_lse<float, 128>(st, L, P, q, k, Hq, Hkv, scale, row_lse, ws)
-                  : run_row_lse<float, 64>(st, L, P, q, k, Hq, Hkv, scale, row_lse, ws);
+    return d == 128 ? run_row_lse<__bf16, 128>(st, L, P, q, k, Hq, Hkv, scale, row_lse, lse2, ws)
+                    : run_row_lse<__bf16, 64>(st, L, P, q, k, Hq, Hkv, scale, row_lse, lse2, ws);
+  return d == 128 ? run_row_lse<float, 128>(st, L, P, q, k, Hq, Hkv, scale, row_lse, lse2, ws)
+                  : run_row_lse<float, 64>(st, L, P, q, k, Hq, Hkv, scale, row_lse, lse2, ws);
+}
+
+hipError_t launch_lse_to_log2(hipStream_t st, int rows, const float *lse, float *lse2) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(lse_to_log2_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, lse, rows, lse2);
+  return hipGetLastError();
 }
 
 hipError_t launch_colsum(hipStream_t st, const DevLayout &L, const AttnPlan &P, int dtype,
                          const void *q, const void *k, int Hq, int Hkv, int d, float scale,
-                         const float *row_lse, char *ws) {
+                         const float *lse2, char *ws) {
   if (dtype == AVTP_BF16)
-    return d == 128 ? run_colsum<__bf16, 128>(st, L, P, q, k, Hq, Hkv, scale, row_lse, ws)
-                    : run_colsum<__bf16, 64>(st, L, P, q, k, Hq, Hkv, scale, row_lse, ws);
-  return d == 128 ? run_colsum<float, 128>(st, L, P, q, k, Hq, Hkv, scale, row_lse, ws)
-                  : run_colsum<float, 64>(st, L, P, q, k, Hq, Hkv, scale, row_lse, ws);
+    return d == 128 ? run_colsum<__bf16, 128>(st, L, P, q, k, Hq, Hkv, scale, lse2, ws)
+                    : run_colsum<__bf16, 64>(st, L, P, q, k, Hq, Hkv, scale, lse2, ws);
+  return d == 128 ? run_colsum<float, 128>(st, L, P, q, k, Hq, Hkv, scale, lse2, ws)
+                  : run_colsum<float, 64>(st, L, P, q, k, Hq, Hkv, scale, lse2, ws);
 }
 
 hipError_t launch_finalize(hipStream_t st, const DevLayout &L, const float *colsum, int Hq,
