@@ -182,11 +182,13 @@ __device__ inline void interleave_mfma_valu() {
   }
 }
 
-// Scheduling hint for one pass-1 key tile: per k-step the NT MFMAs of the
-// step, each followed by up to V VALU ops working on the previous tile, then
-// one LDS read of a later step's fragment.
-template <int NS, int NT, int V>
+// Scheduling hint for one pass-1 key tile: the LDS reads of the first PF
+// k-steps (unless the compiler hoisted them out of the tile), then per k-step
+// the NT MFMAs of the step, each followed by up to V VALU ops working on the
+// previous tile, then the LDS read of the fragment PF steps ahead.
+template <int NS, int NT, int V, int PF>
 __device__ inline void interleave_tile() {
+  __builtin_amdgcn_sched_group_barrier(0x100, PF, 0);  // DS read
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
 #pragma unroll
@@ -194,7 +196,7 @@ __device__ inline void interleave_tile() {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // VALU
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    if (s + PF < NS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
   }
 }
 
@@ -206,17 +208,13 @@ __device__ inline F load_frag(const char *p) {
   return *reinterpret_cast<const F *>(p);
 }
 
-// Positions spanned by query rows [r0, r1) of one (sequence, key head);
-// row r is text row t = r % Tb of head r / Tb, positions ascend with t.
-__device__ inline void rows_pos_range(const int32_t *tp, int Tb, int r0, int r1, int &pmin,
+// Positions spanned by pass-1 query rows [r0, r1) of one (sequence, key
+// head).  Rows are token-major: row r is text token r / G under query head
+// r % G of the group, so positions ascend with r.
+__device__ inline void rows_pos_range(const int32_t *tp, int G, int r0, int r1, int &pmin,
                                       int &pmax) {
-  if (r0 / Tb == (r1 - 1) / Tb) {
-    pmin = tp[r0 % Tb];
-    pmax = tp[(r1 - 1) % Tb];
-  } else {
-    pmin = tp[0];
-    pmax = tp[Tb - 1];
-  }
+  pmin = tp[r0 / G];
+  pmax = tp[(r1 - 1) / G];
 }
 
 struct P1Args {
@@ -239,7 +237,9 @@ struct P1Args {
 // reference of a row is kept lazily: it is raised (and the row's sum
 // rescaled) only when a 16-term chain exceeds 2^64, which the exact
 // recomputation of that chain then resolves.  A tile that some lane sees
-// only in part takes a per-element masked variant.
+// only in part takes a per-element masked variant.  Query rows are
+// token-major (the G heads of one text token adjacent), so a block's rows
+// span few positions and a block of early text rows stops at its last row.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Args a) {
   using G_ = Geo<T, D>;
@@ -273,12 +273,12 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   const size_t HqT = (size_t)a.Hq * a.T_tot;
   const int32_t *tp = a.text_pos + t0;
   int bmin = 0, bmax = -1;
-  if (kbeg < L) rows_pos_range(tp, Tb, row0, min(R, row0 + QB), bmin, bmax);
+  if (kbeg < L) rows_pos_range(tp, a.G, row0, min(R, row0 + QB), bmin, bmax);
   if (kbeg >= L || s0 + kbeg > bmax) {
     // no row of the block sees a key of the chunk: empty partials, so that
     // the combine can read every chunk of every row
     for (int r = row0 + (int)threadIdx.x; r < min(R, row0 + QB); r += kThreads) {
-      const int hh = r / Tb, qidx = (g * a.G + hh) * a.T_tot + t0 + (r - hh * Tb);
+      const int t = r / a.G, qidx = (g * a.G + (r - t * a.G)) * a.T_tot + t0 + t;
       a.part_m[kc * HqT + qidx] = -INFINITY;
       a.part_l[kc * HqT + qidx] = 0.f;
     }
@@ -293,7 +293,7 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   const int wr0 = row0 + wave * NT * 32;
   const bool active = wr0 < R;
   int wmin = 0, wmax = -1;
-  if (active) rows_pos_range(tp, Tb, wr0, min(R, wr0 + NT * 32), wmin, wmax);
+  if (active) rows_pos_range(tp, a.G, wr0, min(R, wr0 + NT * 32), wmin, wmax);
 
   // stationary operand: this wave's query rows
   frag qf[NT][NS];
@@ -303,7 +303,7 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
     const int r = wr0 + i * 32 + col;
     qrel[i] = -1;
     if (r < R) {
-      const int hh = r / Tb, t = r - hh * Tb, h = g * a.G + hh;
+      const int t = r / a.G, h = g * a.G + (r - t * a.G);
       qrel[i] = tp[t] - s0;
       const char *src = a.q + ((size_t)(t0 + t) * a.Hq + h) * ROWB + hi * E * sizeof(T);
 #pragma unroll
@@ -353,14 +353,18 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   for (int i = 0; i < 2 * NT; ++i) acc[i] = f32x16{};
   constexpr int kNone = 1 << 30;  // pend_kb of an empty pending tile: no lane sees it
   int pend_kb = kNone;
+  constexpr int kAllOrNone = 1, kPerElem = 2;
+  using AllOrNone = std::integral_constant<int, kAllOrNone>;
+  using PerElem = std::integral_constant<int, kPerElem>;
 
   // One key tile: MFMAs of the tile at buf row `lrow` into the sets of
   // parity P (if MF), and the exp2 sums of the pending tile (sets of parity
-  // P^1), unmasked (every lane sees all or none of it) or per element.
-  auto tile = [&](const char *buf, int lrow, auto par_tag, auto masked_tag, auto mf_tag)
+  // P^1).  Mode M: kAllOrNone (every lane sees all or none of the pending
+  // tile) or kPerElem (per-element mask).
+  auto tile = [&](const char *buf, int lrow, auto par_tag, auto mode_tag, auto mf_tag)
       __attribute__((always_inline)) {
     constexpr int P = decltype(par_tag)::value;
-    constexpr bool MASKED = decltype(masked_tag)::value;
+    constexpr int M = decltype(mode_tag)::value;
     constexpr bool MF = decltype(mf_tag)::value;
     constexpr int CS = P * NT, PS = (P ^ 1) * NT;
     int vl[NT];
@@ -369,8 +373,6 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
     for (int qi = 0; qi < NT; ++qi) {
       vl[qi] = vlimit(qi, pend_kb);
       r[qi] = ref[qi];
-      ts[qi][0] = 0.f;
-      ts[qi][1] = 0.f;
     }
     if (MF) {
 #pragma unroll
@@ -397,18 +399,20 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
 #pragma unroll
         for (int e = (s * 16) / NS; e < ((s + 1) * 16) / NS; ++e) {
           float x = acc[PS + qi][e];
-          if (MASKED) x = eoff(e) <= vl[qi] ? x : -INFINITY;
-          ts[qi][e & 1] += __builtin_amdgcn_exp2f(x * cl2e - r[qi]);
+          if (M == kPerElem) x = eoff(e) <= vl[qi] ? x : -INFINITY;
+          const float v = __builtin_amdgcn_exp2f(x * cl2e - r[qi]);
+          if (e < 2) ts[qi][e] = v;  // each of the two chains starts at its first term
+          else ts[qi][e & 1] += v;
         }
       }
     }
-    if (MF) interleave_tile<NS, NT, ((MASKED ? 64 : 48) / NS > 0 ? (MASKED ? 64 : 48) / NS : 1)>();
+    if (MF) interleave_tile<NS, NT, ((M == kPerElem ? 64 : 48) / NS > 0 ? (M == kPerElem ? 64 : 48) / NS : 1), PF>();
     float t[NT];
     bool bad = false;
 #pragma unroll
     for (int qi = 0; qi < NT; ++qi) {
       t[qi] = ts[qi][0] + ts[qi][1];
-      if (!MASKED && vl[qi] < 0) t[qi] = 0.f;  // lane sees none of the pending tile
+      if (M == kAllOrNone && vl[qi] < 0) t[qi] = 0.f;  // lane sees none of the pending tile
       bad = bad || !(t[qi] <= kLazyLimit);
     }
     if (__ballot(bad) != 0ull) {
@@ -455,12 +459,14 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
       auto one = [&](auto kt_tag) __attribute__((always_inline)) {
         constexpr int KT = decltype(kt_tag)::value;
         using par_tag = std::integral_constant<int, KT & 1>;
-        // a lane that sees only part of the pending tile needs the masked variant
+        // a lane that sees only part of the pending tile needs the masked
+        // variant (this check also covers the latency of the tile's first
+        // LDS reads)
         bool part = false;
 #pragma unroll
         for (int qi = 0; qi < NT; ++qi) part = part || (unsigned)(qrel[qi] - pend_kb) < 31u;
-        if (__ballot(part) == 0ull) tile(buf, KT * 32, par_tag{}, std::false_type{}, std::true_type{});
-        else tile(buf, KT * 32, par_tag{}, std::true_type{}, std::true_type{});
+        if (__ballot(part) == 0ull) tile(buf, KT * 32, par_tag{}, AllOrNone{}, std::true_type{});
+        else tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{});
         pend_kb = ks + KT * 32;
       };
       static_assert(TPS == 2 || TPS == 4, "one stage is two or four key tiles");
@@ -476,10 +482,10 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
         constexpr int KT = decltype(kt_tag)::value;
         using par_tag = std::integral_constant<int, KT & 1>;
         if (st * TPS + KT < ntw) {
-          tile(buf, KT * 32, par_tag{}, std::true_type{}, std::true_type{});
+          tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{});
           pend_kb = ks + KT * 32;
         } else if (st * TPS + KT == ntw) {
-          tile(buf, 0, par_tag{}, std::true_type{}, std::false_type{});
+          tile(buf, 0, par_tag{}, PerElem{}, std::false_type{});
           pend_kb = kNone;
         }
       };
@@ -497,7 +503,7 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   }
   if (!active) return;
   // with a whole number of stages the pending tile is the last (odd) one
-  if (ntw > 0 && ntw % TPS == 0) tile(smA, 0, P0{}, std::true_type{}, std::false_type{});
+  if (ntw > 0 && ntw % TPS == 0) tile(smA, 0, P0{}, PerElem{}, std::false_type{});
 
   // merge the two half-waves (same query column, disjoint keys) and store
 #pragma unroll
@@ -510,7 +516,7 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
             (om == -INFINITY ? 0.f : ol * __builtin_amdgcn_exp2f(om - nm));
     const int r = wr0 + i * 32 + col;
     if (hi == 0 && r < R) {
-      const int hh = r / Tb, qidx = (g * a.G + hh) * a.T_tot + t0 + (r - hh * Tb);
+      const int t = r / a.G, qidx = (g * a.G + (r - t * a.G)) * a.T_tot + t0 + t;
       a.part_m[kc * HqT + qidx] = nm;
       a.part_l[kc * HqT + qidx] = tot;
     }
