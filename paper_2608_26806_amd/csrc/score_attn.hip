@@ -167,6 +167,39 @@ struct DmaPlan {
                                        (__attribute__((address_space(3))) void *)(lds + gi * 1024), 16, 0, 0);
     }
   }
+  // Token-major rows: row r of the source is token r >> lg, head r & (G-1)
+  // (G = 2^lg), at byte offset (r >> lg) * tok + (r & (G-1)) * ROWB.  The
+  // rows of one wave load start at a multiple of RPL, so the offset of row
+  // r0 + lane/NCH splits into a part of r0 and a lane part (no carries for
+  // any power-of-two G).
+  __device__ static inline void lane_offsets_tm(uint32_t (&lo)[PER], int lane, int lg, uint32_t tok) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int lr = lane / NCH, r = j * RPL + lr;
+      lo[j] = (uint32_t)(lr >> lg) * tok + (uint32_t)(lr & ((1 << lg) - 1)) * G_::ROWB +
+              (uint32_t)(((lane % NCH) ^ (r & G_::SWZ)) * 16);
+    }
+  }
+  // rows [r0, r0 + ROWS) of a token-major source (r0 a multiple of ROWS)
+  __device__ static inline void issue_tm(char *lds, const char *base, int r0, int wave,
+                                         const uint32_t (&lo)[PER], int lg, uint32_t tok) {
+    int w = wave;
+    asm volatile("" : "+s"(w));
+    uint32_t l[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      l[j] = lo[j];
+      asm volatile("" : "+v"(l[j]));
+    }
+#pragma unroll
+    for (int i = 0; i < DMA; ++i) {
+      const int gi = w * DMA + i;
+      const int rr = r0 + w * (ROWS / 4) + i * RPL;
+      const char *row = base + (uint32_t)(rr >> lg) * tok + (uint32_t)(rr & ((1 << lg) - 1)) * G_::ROWB;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(row + l[i % PER]),
+                                       (__attribute__((address_space(3))) void *)(lds + gi * 1024), 16, 0, 0);
+    }
+  }
 };
 
 // Scheduling hint for one MFMA chain of NS steps sharing a basic block with
@@ -655,52 +688,42 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   const uint32_t qstride = (uint32_t)a.Hq * ROWB;
   const float *lbase = a.lse2 + (size_t)g * a.G * a.T_tot + t0;    // head g*G, text row 0
   using DP = DmaPlan<T, D, QR>;
-  // One stage: query rows, their LSE and positions.  Wave 0 loads the LSE,
-  // wave 1 the positions, 64 rows per instruction.  (hh, toff): head and
-  // text row of the stage's first row rs.
-  auto issue_stage = [&](int rs, int hh, int toff, QTile2<ROWB> &dst) __attribute__((always_inline)) {
-    const bool one_head = rs + QR <= r_hi && toff + QR <= Tb;
-    if (one_head) {  // consecutive text rows of one head
+  // Rows are token-major: row r is text token r / G under query head
+  // g*G + r % G, so positions ascend with r.  With G a power of two every
+  // stage load has per-lane offsets fixed across stages.
+  const int lg = __builtin_ctz((unsigned)a.G);
+  const bool g_pow2 = (a.G & (a.G - 1)) == 0;
+  // One stage: query rows [rs, rs + QR), their LSE and positions.  Wave 0
+  // loads the LSE, wave 1 the positions, 64 rows per instruction.
+  auto issue_stage = [&](int rs, QTile2<ROWB> &dst) __attribute__((always_inline)) {
+    if (g_pow2 && rs + QR <= R) {
       int ln = lane;
       asm volatile("" : "+v"(ln));
       uint32_t dlo[DP::PER];
-      DP::lane_offsets(dlo, ln, qstride);
-      DP::issue(dst.q, qbase + ((size_t)toff * a.Hq + hh) * ROWB, wave, dlo, qstride);
+      DP::lane_offsets_tm(dlo, ln, lg, qstride);
+      DP::issue_tm(dst.q, qbase, rs, wave, dlo, lg, qstride);
     } else {
       dma_stage<T, D, QR>(dst.q, qbase, wave, lane, [&](int row) __attribute__((always_inline)) {
         const int r = min(rs + row, R - 1);  // rows past R re-read row R-1; their lse is +inf
-        const int h2 = r / Tb, t = r - h2 * Tb;
-        return (uint32_t)(t * a.Hq + h2) * ROWB;
+        const int t = r / a.G;
+        return (uint32_t)(t * a.Hq + (r - t * a.G)) * ROWB;
       });
     }
     if (wave < 2) {
 #pragma unroll
       for (int i = 0; i < QR / 64; ++i) {
+        const int r = rs + i * 64 + lane;
         const void *src;
-        if (one_head) {
-          const int t = toff + i * 64 + lane;
-          src = wave == 0 ? (const void *)(lbase + (size_t)hh * a.T_tot + t) : (const void *)(tp + t);
+        if (r < r_hi) {
+          const int t = r / a.G;
+          src = wave == 0 ? (const void *)(lbase + (size_t)(r - t * a.G) * a.T_tot + t) : (const void *)(tp + t);
         } else {
-          const int r = rs + i * 64 + lane;
-          if (r < r_hi) {
-            const int h2 = r / Tb, t = r - h2 * Tb;
-            src = wave == 0 ? (const void *)(lbase + (size_t)h2 * a.T_tot + t) : (const void *)(tp + t);
-          } else {
-            src = wave == 0 ? (const void *)&kRowNone : (const void *)&kPosNone;
-          }
+          src = wave == 0 ? (const void *)&kRowNone : (const void *)&kPosNone;
         }
         void *dstp = wave == 0 ? (void *)(dst.lse + i * 64) : (void *)(dst.pos + i * 64);
         __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
                                          (__attribute__((address_space(3))) void *)dstp, 4, 0, 0);
       }
-    }
-  };
-  // the text row index of the row QR rows further, and its head
-  auto advance = [&](int &hh, int &toff) __attribute__((always_inline)) {
-    toff += QR;
-    while (toff >= Tb) {
-      toff -= Tb;
-      ++hh;
     }
   };
 
@@ -778,7 +801,11 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
     for (int e = 0; e < 16; ++e) plv[e] = INFINITY;
   };
   // a sub-tile in slot U some rows of which see only part of the wave's
-  // keys: settle what is pending, then MFMAs and masked terms, unpipelined
+  // keys: settle what is pending, then MFMAs and masked terms, unpipelined.
+  // The terms are summed in the order of the unmasked path (two alternating
+  // partial sums per chain, elements ascending) and a masked term is an
+  // exact 0, so a key that sees every row of the sub-tile gets the same bits
+  // on either path.
   auto sub_masked = [&](const QTile2<ROWB> &cur, auto u_tag) __attribute__((always_inline)) {
     constexpr int U = decltype(u_tag)::value;
     settle();
@@ -791,54 +818,47 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
 #pragma unroll
       for (int s = 0; s < NS; ++s) acc[j] = MM::run(av[s], kf[j][s], acc[j]);
     }
+    float ts[NKT][2];
+#pragma unroll
+    for (int j = 0; j < NKT; ++j) ts[j][0] = ts[j][1] = 0.f;
 #pragma unroll
     for (int e4 = 0; e4 < 4; ++e4) {
       const int ro = U * 32 + hi * 4 + 8 * e4;
-      const float4 lv = *reinterpret_cast<const float4 *>(&cur.lse[ro]);
-      const int4 qp = *reinterpret_cast<const int4 *>(&cur.pos[ro]);
+      const float4 lv4 = *reinterpret_cast<const float4 *>(&cur.lse[ro]);
+      const int4 qp4 = *reinterpret_cast<const int4 *>(&cur.pos[ro]);
+      const float lv[4] = {lv4.x, lv4.y, lv4.z, lv4.w};
+      const int qp[4] = {qp4.x, qp4.y, qp4.z, qp4.w};
 #pragma unroll
       for (int j = 0; j < NKT; ++j) {
-        const f32x16 &x = acc[j];
         const int kp = kpos(j);
-        float t = kp <= qp.x ? __builtin_amdgcn_exp2f(x[4 * e4 + 0] * cl2e - lv.x) : 0.f;
-        t += kp <= qp.y ? __builtin_amdgcn_exp2f(x[4 * e4 + 1] * cl2e - lv.y) : 0.f;
-        t += kp <= qp.z ? __builtin_amdgcn_exp2f(x[4 * e4 + 2] * cl2e - lv.z) : 0.f;
-        t += kp <= qp.w ? __builtin_amdgcn_exp2f(x[4 * e4 + 3] * cl2e - lv.w) : 0.f;
-        cs[j] += t;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * e4 + i;
+          ts[j][e & 1] += kp <= qp[i] ? __builtin_amdgcn_exp2f(acc[j][e] * cl2e - lv[i]) : 0.f;
+        }
       }
     }
+#pragma unroll
+    for (int j = 0; j < NKT; ++j) cs[j] += ts[j][0] + ts[j][1];
   };
 
   const int nstage = (r_hi - r_lo + QR - 1) / QR;
-  int ch = r_lo / Tb, ct = r_lo - ch * Tb;  // head and text row of the current stage's first row
-  if (nstage > 0) issue_stage(r_lo, ch, ct, qtA);
+  if (nstage > 0) issue_stage(r_lo, qtA);
   auto step = [&](QTile2<ROWB> &cur, QTile2<ROWB> &nxt, int st) __attribute__((always_inline)) {
     const int rs = r_lo + st * QR;
-    int nh = ch, nt = ct;
-    advance(nh, nt);
     wait_vmem();
     __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
-    if (st + 1 < nstage) issue_stage(rs + QR, nh, nt, nxt);
+    if (st + 1 < nstage) issue_stage(rs + QR, nxt);
     if (active) {
       auto one = [&](auto u_tag) __attribute__((always_inline)) {
         constexpr int U = decltype(u_tag)::value;
-        const int r0 = rs + U * 32;
-        const int nv = min(32, r_hi - r0);  // valid rows of the sub-tile
-        int tt = ct + U * 32;               // its first text row, within its head
-        while (tt >= Tb) tt -= Tb;
-        int qmin = 0x7fffffff, qmax = -1;
+        const int nv = min(32, r_hi - (rs + U * 32));  // valid rows of the sub-tile
         if (nv > 0) {
-          if (tt + nv <= Tb) {  // one head: positions ascend
-            qmin = cur.pos[U * 32];
-            qmax = cur.pos[U * 32 + nv - 1];
-          } else {  // crosses a head boundary: classify as seen in part
-            qmin = -1;
-            qmax = 0x7ffffffe;
+          const int qmin = cur.pos[U * 32], qmax = cur.pos[U * 32 + nv - 1];
+          if (qmax >= kmin) {  // else no row of the sub-tile sees a key of the wave
+            if (qmin >= kmax) sub_tile(cur, u_tag);
+            else sub_masked(cur, u_tag);
           }
-        }
-        if (qmax >= kmin) {  // else no row of the sub-tile sees a key of the wave
-          if (qmin >= kmax) sub_tile(cur, u_tag);
-          else sub_masked(cur, u_tag);
         }
       };
       one(std::integral_constant<int, 0>{});
@@ -846,8 +866,6 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
       one(std::integral_constant<int, 2>{});
       one(std::integral_constant<int, 3>{});
     }
-    ch = nh;
-    ct = nt;
   };
   for (int st = 0; st < nstage; st += 2) {
     step(qtA, qtB, st);
