@@ -289,13 +289,16 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   __shared__ __attribute__((aligned(16))) char smB[KS * ROWB];
 
   // Blocks that share one key chunk (the nqb query blocks of a unit) get
-  // ids that are equal mod 8, i.e. land on one XCD and share its L2.
-  const int nunits = a.B * a.Hkv * a.nkc;
+  // ids that are equal mod 8, i.e. land on one XCD and share its L2.  Units
+  // are numbered (sequence, key head) fastest, so each XCD gets every chunk
+  // of its heads (chunks differ in work: the last is short, early text rows
+  // see only the first ones) and the short last chunks are dispatched last.
+  const int nbg = a.B * a.Hkv, nunits = nbg * a.nkc;
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
   const int qb = local % a.nqb;
   const int unit = (local / a.nqb) * 8 + xcd;
   if (unit >= nunits) return;
-  const int kc = unit % a.nkc, bg = unit / a.nkc, g = bg % a.Hkv, b = bg / a.Hkv;
+  const int kc = unit / nbg, bg = unit - kc * nbg, g = bg % a.Hkv, b = bg / a.Hkv;
 
   const int s0 = a.cu_seqlens[b], L = a.cu_seqlens[b + 1] - s0;
   const int t0 = a.cu_text[b], Tb = a.cu_text[b + 1] - t0;
