@@ -28,6 +28,8 @@ struct AttnPlan {
   int nkc;        // chunks per sequence (max)
   int nkb;        // key blocks per (sequence, key head) in pass 2
   int nqs;        // query splits of pass 2 (column-sum planes per key head)
+  int nsl;        // pass 2: each (sequence, key head)'s key blocks are dealt to nsl
+                  // slices (kb mod nsl), so that there are units for all 8 XCDs
   size_t off_part_m, off_part_l, off_lse, off_lse2, off_colsum, bytes;
 };
 

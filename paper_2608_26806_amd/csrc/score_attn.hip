@@ -605,6 +605,7 @@ struct P2Args {
   const float *lse2;  // row LSE in log2 units, [Hq][T_tot]
   const int32_t *cu_seqlens, *cu_text, *text_pos;
   int B, Hq, Hkv, G, T_tot, N_tok, nkb, nqs;
+  int nsl, ppx, kps;  // key-block slices per unit, (unit, slice) pairs per XCD, blocks per pair
   float cl2e;
   float *colsum;  // [nqs][Hkv][N_tok]
 };
@@ -637,15 +638,21 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   // two query buffers as distinct objects (see pass 1)
   __shared__ QTile2<ROWB> qtA, qtB;
 
-  // the key blocks of one (sequence, key head, query split) read the same
-  // queries: keep them on one XCD
-  const int nunits = a.B * a.Hkv;
-  const int per = a.nkb * a.nqs;
+  // The key blocks of one (sequence, key head) read the same queries, so
+  // they stay on few XCDs: a unit's key blocks are dealt to nsl slices
+  // (kb mod nsl, enough (unit, slice) pairs for the 8 XCDs), and the blocks
+  // of one pair land on XCD pair mod 8.  On an XCD the pairs take turns, key
+  // block by key block: blocks early in a sequence are seen by more text rows
+  // (heavier), so the lightest ones are dispatched last.
+  const int npairs = a.B * a.Hkv * a.nsl;
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-  const int wi = local % per;
-  const int unit = (local / per) * 8 + xcd;
-  if (unit >= nunits) return;
-  const int kb = wi % a.nkb, qsp = wi / a.nkb;
+  const int pj = local % a.ppx, kk = local / a.ppx;
+  const int pair = pj * 8 + xcd;
+  if (pair >= npairs) return;
+  const int unit = pair / a.nsl, sl = pair - unit * a.nsl;
+  const int kbl = kk % a.kps, qsp = kk / a.kps;
+  const int kb = kbl * a.nsl + sl;
+  if (kb >= a.nkb || qsp >= a.nqs) return;
   const int g = unit % a.Hkv, b = unit / a.Hkv;
   const int s0 = a.cu_seqlens[b], L = a.cu_seqlens[b + 1] - s0;
   const int t0 = a.cu_text[b], Tb = a.cu_text[b + 1] - t0;
@@ -998,8 +1005,10 @@ hipError_t run_colsum(hipStream_t st, const DevLayout &L, const AttnPlan &P, con
   a.nqs = P.nqs;
   a.cl2e = scale * kLog2e;
   a.colsum = (float *)(ws + P.off_colsum);
-  const int nunits = L.B * Hkv;
-  const int grid = ((nunits + 7) / 8) * 8 * P.nkb * P.nqs;
+  a.nsl = P.nsl;
+  a.ppx = (L.B * Hkv * P.nsl + 7) / 8;
+  a.kps = (P.nkb + P.nsl - 1) / P.nsl;
+  const int grid = 8 * a.ppx * a.kps * P.nqs;
   hipLaunchKernelGGL((colsum_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
@@ -1029,6 +1038,16 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   if (P.nkc < 1) P.nkc = 1;
   P.nkb = (L.max_seqlen + keys_per_block - 1) / keys_per_block;
   if (P.nkb < 1) P.nkb = 1;
+  {  // slices per unit: the fewest that make the (unit, slice) pairs a multiple of 8
+    int a8 = L.B * Hkv, b8 = 8;
+    while (b8 != 0) {
+      const int t = a8 % b8;
+      a8 = b8;
+      b8 = t;
+    }
+    P.nsl = 8 / a8;
+    if (P.nsl > P.nkb) P.nsl = P.nkb;
+  }
   // Split the query rows of pass 2 only when its grid would not fill the
   // chip twice over (512 blocks): a block pays for loading its keys and for
   // filling its pipeline, so fewer, longer blocks are faster; keep at least
