@@ -641,12 +641,12 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   // The key blocks of one (sequence, key head) read the same queries, so
   // they stay on few XCDs: a unit's key blocks are dealt to nsl slices
   // (kb mod nsl, enough (unit, slice) pairs for the 8 XCDs), and the blocks
-  // of one pair land on XCD pair mod 8.  On an XCD the pairs take turns, key
-  // block by key block: blocks early in a sequence are seen by more text rows
-  // (heavier), so the lightest ones are dispatched last.
+  // of one pair land on XCD pair mod 8, one pair after the other, so that
+  // an XCD's L2 holds the queries of few units at a time.
   const int npairs = a.B * a.Hkv * a.nsl;
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-  const int pj = local % a.ppx, kk = local / a.ppx;
+  const int per = a.kps * a.nqs;
+  const int kk = local % per, pj = local / per;
   const int pair = pj * 8 + xcd;
   if (pair >= npairs) return;
   const int unit = pair / a.nsl, sl = pair - unit * a.nsl;
