@@ -379,3 +379,52 @@ def compact(keep_idx, x: np.ndarray, axis: int = 0) -> np.ndarray:
     """out[r] = x[keep_idx[r]] along the token axis; values are copied unchanged
     (position ids keep their original values)."""
     return np.take(x, np.asarray(keep_idx, dtype=np.int64), axis=axis)
+
+
+# ---------------------------------------------------------------------------
+# O5: architecture-aware pruning-layer selection (Sec. 3.3.2)
+# ---------------------------------------------------------------------------
+def layer_attention(layout, img_sum) -> np.ndarray:
+    """A^(b) of one layer for every sequence (sample) b: the attention the layer
+    pays to all visual tokens of the sample (Sec. 3.3.2, the A_l equation).
+
+    With the per-token attention score s_j of ``attn_scores`` standing for
+    Attention(l, v_j), the sum over the sample's visual tokens equals the sum of
+    its per-image sums S_i.  Summed exactly (math.fsum) from the float32 S_i."""
+    cu = np.asarray(layout.cu_img, dtype=np.int64)
+    s = np.asarray(img_sum, dtype=np.float64)
+    return np.array([math.fsum(s[cu[b]:cu[b + 1]].tolist()) for b in range(len(cu) - 1)],
+                    dtype=np.float64)
+
+
+def layer_ranks(A) -> np.ndarray:
+    """Rank(A_l^(i)) of Sec. 3.3.2 for A [L, N] (layer l, sample i): within each
+    sample the layers are ranked by attention, rank 1 = the largest.
+
+    Readings: equal values rank the lower layer index first, so every sample's
+    ranks are a permutation of 1..L; NaN counts as the smallest value; -0.0
+    equals +0.0."""
+    A = np.asarray(A, dtype=np.float64)
+    L, N = A.shape
+    ranks = np.zeros((L, N), dtype=np.int64)
+    for i in range(N):
+        v = [-math.inf if math.isnan(x) else float(x) for x in A[:, i]]
+        order = sorted(range(L), key=lambda l: (-v[l], l))
+        for r, l in enumerate(order):
+            ranks[l, i] = r + 1
+    return ranks
+
+
+def layer_select(A, k: int):
+    """R_l = (1/N) sum_i Rank(A_l^(i)) and the k pruning layers with the highest
+    average attention, i.e. the smallest average rank (Sec. 3.3.2, the R_l
+    equation and the top-k rule).
+
+    Returns (rank_sum [L] int64 = N R_l exactly, R [L] float64, selected: the k
+    chosen layer indices in ascending order).  Equal rank sums choose the lower
+    layer index."""
+    ranks = layer_ranks(A)
+    L, N = ranks.shape
+    rank_sum = ranks.sum(axis=1)
+    order = sorted(range(L), key=lambda l: (int(rank_sum[l]), l))
+    return rank_sum, rank_sum / float(N), sorted(order[:k])
