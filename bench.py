@@ -73,6 +73,30 @@ def measured_traffic(kernel, workload, src_path):
     return None
 
 
+def time_layer_selection(dl, isum, stream, dev, reps: int = 50) -> dict:
+    """Median times of the calibration calls of Sec. 3.3.2 (not part of a pruning
+    layer's step): the per-sample attention of one layer on this workload's image
+    sums, and the ranking of a 36-layer x 400-sample table (100 samples from each
+    of 4 benchmarks, a 36-layer model), k = 4."""
+    rng = np.random.default_rng(36400)
+    table = torch.from_numpy(rng.standard_normal((36, 400)).astype(np.float32)).to(dev)
+    a_out = torch.empty(max(1, dl.B), dtype=torch.float32, device=dev)
+    rs = torch.empty(36, dtype=torch.int32, device=dev)
+    sel = torch.empty(4, dtype=torch.int32, device=dev)
+    res = {}
+    for name, fn in [("layer_attention_us", lambda: A.layer_attention(dl, isum, out=a_out)),
+                     ("layer_select_us_36x400_k4", lambda: A.layer_select(table, 4, rs, sel))]:
+        fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+        for r in range(reps):
+            ev[2 * r].record(stream)
+            fn()
+            ev[2 * r + 1].record(stream)
+        torch.cuda.synchronize()
+        res[name] = float(np.median([ev[2 * r].elapsed_time(ev[2 * r + 1]) for r in range(reps)])) * 1e3
+    return res
+
+
 def algorithmic_counts(lay, Hq, d, row_bytes_total):
     """Per-launch algorithmic work of each stage.
 
@@ -237,6 +261,8 @@ def main():
     if st.any():
         print(f"warning: device status flags {st.tolist()}", file=sys.stderr)
 
+    layer_sel = time_layer_selection(dl, isum, stream, dev)
+
     M = int(lay.img_len.sum())
     ms_layer = float(np.median(layer_ms))
     ms = {n: float(np.mean(per[:, j])) for j, n in enumerate(names)}
@@ -289,6 +315,7 @@ def main():
                              "unit": "GB/s", "frac": comp_gbs / PEAK_HBM_GBS,
                              "alg_bytes": comp_bytes},
         "select_plus_compact_hbm_frac": selcomp_gbs / PEAK_HBM_GBS,
+        "layer_selection": layer_sel,
         "wall_s_timed_region": wall,
         "input_generation_s": gen_s,
     }

@@ -68,6 +68,8 @@ typedef enum {
 #define AVTP_MAX_IMAGES 8192
 #define AVTP_MAX_IMAGE_LEN (1 << 20)
 #define AVTP_MAX_TENSORS 8
+#define AVTP_MAX_LAYERS 1024       /* avtp_layer_select: layers               */
+#define AVTP_MAX_SAMPLES (1 << 20) /* avtp_layer_select: samples              */
 
 /*
  * Packed ("THD") description of one batch of B sequences, N_tok tokens.
@@ -197,6 +199,39 @@ int avtp_select(avtp_stream_t stream, const avtp_layout *layout, const float *sc
  * ---------------------------------------------------------------------- */
 int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,
                  int64_t n_out, const avtp_tensor *tensors, int n_tensors);
+
+/* ------------------------------------------------------------------------
+ * Architecture-aware pruning-layer selection (Sec. 3.3.2), computed from
+ * calibration prefills.  For sample i and layer l the paper sums the
+ * attention the layer pays to every visual token,
+ *   A_l^(i) = sum_j Attention(l, v_j^(i)),
+ * ranks the layers within each sample, averages the ranks over the N samples,
+ *   R_l = 1/N sum_i Rank(A_l^(i)),
+ * and prunes at the k layers of highest average attention.
+ *
+ * avtp_layer_attention -- A of one layer for every sequence of a batch (each
+ * sequence is one sample): A_out[b] = sum of img_sum over the images of
+ * sequence b (img_sum from avtp_score in AVTP_SCORE_ATTN mode, whose
+ * per-token score stands for Attention(l, v_j)), accumulated in float64 in
+ * image order and rounded once to fp32; 0 for a sequence without images.
+ *   img_sum [n_img] fp32 (device), A_out [B] fp32 (device; typically row l
+ *   of the caller's [L][N] table, at the batch's sample offset).
+ *
+ * avtp_layer_select -- ranks and selection from the whole table.
+ *   A [L][N] fp32 (device, row-major: layer l, sample i at A[l*N + i]);
+ *   1 <= L <= AVTP_MAX_LAYERS, 1 <= N <= AVTP_MAX_SAMPLES, 1 <= k <= L.
+ *   Within each sample, rank 1 is the largest A; equal values rank the lower
+ *   layer index first (each sample's ranks are a permutation of 1..L); NaN
+ *   ranks as the smallest value; -0.0 equals +0.0.
+ *   rank_sum [L] int32 (device, output): sum_i Rank(A_l^(i)) = N * R_l exactly.
+ *   selected [k] int32 (device, output): the k layers with the smallest rank
+ *   sums (equal sums: lower layer index first), in ascending layer order.
+ * Both calls: AVTP_ERR_INVALID_ARG for null pointers or sizes out of range.
+ * ---------------------------------------------------------------------- */
+int avtp_layer_attention(avtp_stream_t stream, const avtp_layout *layout, const float *img_sum,
+                         float *A_out);
+int avtp_layer_select(avtp_stream_t stream, const float *A, int L, int N, int k,
+                      int32_t *rank_sum, int32_t *selected);
 
 /* Human-readable name of an avtp_status value (static string). */
 const char *avtp_status_string(int status);

@@ -72,10 +72,13 @@ def lib() -> ctypes.CDLL:
         L.avtp_budget.argtypes = [vp, LP, vp, c_int, c_float, c_int, c_int, c_int, vp, vp]
         L.avtp_select.argtypes = [vp, LP, vp, vp, vp, ctypes.c_int64, vp, vp]
         L.avtp_compact.argtypes = [vp, LP, vp, ctypes.c_int64, ctypes.POINTER(_Tensor), c_int]
+        L.avtp_layer_attention.argtypes = [vp, LP, vp, vp]
+        L.avtp_layer_select.argtypes = [vp, vp, c_int, c_int, c_int, vp, vp]
         L.avtp_status_string.argtypes = [c_int]
         L.avtp_status_string.restype = ctypes.c_char_p
         L.avtp_version.restype = c_int
-        for f in ("avtp_score", "avtp_row_lse", "avtp_budget", "avtp_select", "avtp_compact"):
+        for f in ("avtp_score", "avtp_row_lse", "avtp_budget", "avtp_select", "avtp_compact",
+                  "avtp_layer_attention", "avtp_layer_select"):
             getattr(L, f).restype = c_int
         _lib = L
     return _lib
@@ -289,3 +292,30 @@ def compact_new(dl: DeviceLayout, keep_idx: torch.Tensor, srcs: Sequence, stream
         pairs.append((src, dst, tdim))
     compact(dl, keep_idx, pairs, stream=stream)
     return outs
+
+
+# --------------------------------------------------------------------------- layer selection
+def layer_attention(dl: DeviceLayout, img_sum: torch.Tensor, out: Optional[torch.Tensor] = None,
+                    stream=None) -> torch.Tensor:
+    """A [B] fp32: per sequence (sample), the sum of its image sums (one layer)."""
+    if out is None:
+        out = torch.empty(max(1, dl.B), dtype=torch.float32, device=img_sum.device)
+    _check(lib().avtp_layer_attention(_stream(stream), dl.ref(), _ptr(img_sum), _ptr(out)),
+           "avtp_layer_attention")
+    return out[: dl.B]
+
+
+def layer_select(A: torch.Tensor, k: int, rank_sum: Optional[torch.Tensor] = None,
+                 selected: Optional[torch.Tensor] = None, stream=None):
+    """A [L, N] fp32 (layer, sample) -> (rank_sum [L] int32, selected [k] int32 ascending).
+    The average rank R_l is rank_sum / N."""
+    if A.dtype != torch.float32 or A.dim() != 2 or not A.is_contiguous():
+        raise TypeError("A must be a contiguous [L, N] float32 tensor")
+    L, N = A.shape
+    if rank_sum is None:
+        rank_sum = torch.empty(max(1, L), dtype=torch.int32, device=A.device)
+    if selected is None:
+        selected = torch.empty(max(1, k), dtype=torch.int32, device=A.device)
+    _check(lib().avtp_layer_select(_stream(stream), _ptr(A), L, N, int(k), _ptr(rank_sum),
+                                   _ptr(selected)), "avtp_layer_select")
+    return rank_sum[:L], selected[:k]

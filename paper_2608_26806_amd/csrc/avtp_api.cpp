@@ -216,6 +216,23 @@ int avtp_select(avtp_stream_t stream, const avtp_layout *layout, const float *sc
                                   keep_capacity, cu_out, status));
 }
 
+int avtp_layer_attention(avtp_stream_t stream, const avtp_layout *layout, const float *img_sum,
+                         float *A_out) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  if ((L.B > 0 && !A_out) || (L.n_img > 0 && !img_sum)) return AVTP_ERR_INVALID_ARG;
+  return hip_status(launch_layer_attention((hipStream_t)stream, L, img_sum, A_out));
+}
+
+int avtp_layer_select(avtp_stream_t stream, const float *A, int L, int N, int k, int32_t *rank_sum,
+                      int32_t *selected) {
+  if (!A || !rank_sum || !selected) return AVTP_ERR_INVALID_ARG;
+  if (L < 1 || L > AVTP_MAX_LAYERS || N < 1 || N > AVTP_MAX_SAMPLES || k < 1 || k > L)
+    return AVTP_ERR_INVALID_ARG;
+  return hip_status(launch_layer_select((hipStream_t)stream, A, L, N, k, rank_sum, selected));
+}
+
 int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,
                  int64_t n_out, const avtp_tensor *tensors, int n_tensors) {
   DevLayout L;

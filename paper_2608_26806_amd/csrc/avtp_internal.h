@@ -64,4 +64,11 @@ hipError_t launch_select(hipStream_t stream, const DevLayout &L, const float *sc
 hipError_t launch_compact(hipStream_t stream, const DevLayout &L, const int32_t *keep_idx,
                           int64_t n_out, const avtp_tensor *tensors, int n_tensors);
 
+// Pruning-layer selection (Sec. 3.3.2): per-sample attention of one layer,
+// and the per-sample ranks, their sums and the top-k layers.
+hipError_t launch_layer_attention(hipStream_t stream, const DevLayout &L, const float *img_sum,
+                                  float *A);
+hipError_t launch_layer_select(hipStream_t stream, const float *A, int L, int N, int k,
+                               int32_t *rank_sum, int32_t *selected);
+
 }  // namespace avtp

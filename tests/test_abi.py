@@ -136,3 +136,17 @@ def test_compact_descriptor_checks():
 def test_layout_limits():
     lay = build_layout([[1] * 257], 0, 1, 50)         # more images per sequence than supported
     assert _call_score(_dl(lay)) == A.ERR_UNSUPPORTED
+
+
+def test_layer_selection_arguments_rejected_on_host():
+    lib = A.lib()
+    buf = torch.zeros(64, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    assert lib.avtp_layer_select(None, None, 4, 3, 2, p, p) == A.ERR_INVALID_ARG   # no table
+    assert lib.avtp_layer_select(None, p, 0, 3, 1, p, p) == A.ERR_INVALID_ARG      # L = 0
+    assert lib.avtp_layer_select(None, p, 1025, 3, 1, p, p) == A.ERR_INVALID_ARG   # L > max
+    assert lib.avtp_layer_select(None, p, 4, 0, 1, p, p) == A.ERR_INVALID_ARG      # N = 0
+    assert lib.avtp_layer_select(None, p, 4, 3, 5, p, p) == A.ERR_INVALID_ARG      # k > L
+    assert lib.avtp_layer_select(None, p, 4, 3, 0, p, p) == A.ERR_INVALID_ARG      # k = 0
+    assert lib.avtp_layer_attention(None, None, p, p) == A.ERR_INVALID_ARG         # no layout
+    assert lib.avtp_layer_attention(None, _dl().ref(), p, None) == A.ERR_INVALID_ARG
