@@ -78,6 +78,10 @@ def time_layer_selection(dl, isum, stream, dev, reps: int = 50) -> dict:
     layer's step): the per-sample attention of one layer on this workload's image
     sums, and the ranking of a 36-layer x 400-sample table (100 samples from each
     of 4 benchmarks, a 36-layer model), k = 4."""
+    import torch
+
+    from paper_2608_26806_amd import avtp as A
+
     rng = np.random.default_rng(36400)
     table = torch.from_numpy(rng.standard_normal((36, 400)).astype(np.float32)).to(dev)
     a_out = torch.empty(max(1, dl.B), dtype=torch.float32, device=dev)
