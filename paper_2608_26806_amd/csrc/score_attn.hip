@@ -215,13 +215,14 @@ __device__ inline void interleave_mfma_valu() {
   }
 }
 
-// Scheduling hint for one pass-1 key tile: the LDS reads of the first PF
-// k-steps (unless the compiler hoisted them out of the tile), then per k-step
-// the NT MFMAs of the step, each followed by up to V VALU ops working on the
+// Scheduling hint for one pass-1 key tile: the LDS reads of the first LEAD
+// k-steps (none if they were read before the tile), then per k-step the NT
+// MFMAs of the step, each followed by up to V VALU ops working on the
 // previous tile, then the LDS read of the fragment PF steps ahead.
-template <int NS, int NT, int V, int PF>
+template <int NS, int NT, int V, int LEAD>
 __device__ inline void interleave_tile() {
-  __builtin_amdgcn_sched_group_barrier(0x100, PF, 0);  // DS read
+  constexpr int PF = NS < 3 ? NS : 3;
+  if (LEAD > 0) __builtin_amdgcn_sched_group_barrier(0x100, LEAD, 0);  // DS read
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
 #pragma unroll
@@ -397,30 +398,36 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   // parity P (if MF), and the exp2 sums of the pending tile (sets of parity
   // P^1).  Mode M: kAllOrNone (every lane sees all or none of the pending
   // tile) or kPerElem (per-element mask).
-  auto tile = [&](const char *buf, int lrow, auto par_tag, auto mode_tag, auto mf_tag)
+  constexpr int PF = NS < 3 ? NS : 3;  // key fragments are read PF k-steps ahead of their MFMAs
+  frag pf[PF];                          // a tile's first PF fragments, if read before it (PRE)
+  auto tile = [&](const char *buf, int lrow, auto par_tag, auto mode_tag, auto mf_tag, auto pre_tag)
       __attribute__((always_inline)) {
     constexpr int P = decltype(par_tag)::value;
     constexpr int M = decltype(mode_tag)::value;
     constexpr bool MF = decltype(mf_tag)::value;
+    constexpr bool PRE = decltype(pre_tag)::value;
     constexpr int CS = P * NT, PS = (P ^ 1) * NT;
+    // per-element limit (kPerElem); in kAllOrNone a lane sees the whole
+    // pending tile unless its row precedes it, and only lanes that see it
+    // all can take the exact redo below
     int vl[NT];
+    bool none[NT];
     float r[NT], ts[NT][2];
 #pragma unroll
     for (int qi = 0; qi < NT; ++qi) {
-      vl[qi] = vlimit(qi, pend_kb);
+      vl[qi] = M == kPerElem ? vlimit(qi, pend_kb) : 31;
+      none[qi] = qrel[qi] < pend_kb;
       r[qi] = ref[qi];
     }
     if (MF) {
 #pragma unroll
       for (int qi = 0; qi < NT; ++qi) acc[CS + qi] = f32x16{};
     }
-    // key fragments are read PF k-steps ahead of their MFMAs
-    constexpr int PF = NS < 3 ? NS : 3;
     frag av[NS];
     if (MF) {
 #pragma unroll
       for (int s = 0; s < PF; ++s)
-        av[s] = load_frag<frag>(buf + swz_off<T, D>(lrow + col, s * 2 * E + hi * E));
+        av[s] = PRE ? pf[s] : load_frag<frag>(buf + swz_off<T, D>(lrow + col, s * 2 * E + hi * E));
     }
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
@@ -442,13 +449,15 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
         }
       }
     }
-    if (MF) interleave_tile<NS, NT, ((M == kPerElem ? 64 : 48) / NS > 0 ? (M == kPerElem ? 64 : 48) / NS : 1), PF>();
+    if (MF)
+      interleave_tile<NS, NT, ((M == kPerElem ? 64 : 40) / NS > 0 ? (M == kPerElem ? 64 : 40) / NS : 1),
+                      PRE ? 0 : PF>();
     float t[NT];
     bool bad = false;
 #pragma unroll
     for (int qi = 0; qi < NT; ++qi) {
       t[qi] = ts[qi][0] + ts[qi][1];
-      if (M == kAllOrNone && vl[qi] < 0) t[qi] = 0.f;  // lane sees none of the pending tile
+      if (M == kAllOrNone && none[qi]) t[qi] = 0.f;  // lane sees none of the pending tile
       bad = bad || !(t[qi] <= kLazyLimit);
     }
     if (__ballot(bad) != 0ull) {
@@ -498,11 +507,18 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
         // a lane that sees only part of the pending tile needs the masked
         // variant (this check also covers the latency of the tile's first
         // LDS reads)
+        // the tile's first fragments are read before the check, whose VALU
+        // work then covers their latency
+#pragma unroll
+        for (int s = 0; s < PF; ++s)
+          pf[s] = load_frag<frag>(buf + swz_off<T, D>(KT * 32 + col, s * 2 * E + hi * E));
         bool part = false;
 #pragma unroll
         for (int qi = 0; qi < NT; ++qi) part = part || (unsigned)(qrel[qi] - pend_kb) < 31u;
-        if (__ballot(part) == 0ull) tile(buf, KT * 32, par_tag{}, AllOrNone{}, std::true_type{});
-        else tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{});
+        if (__ballot(part) == 0ull)
+          tile(buf, KT * 32, par_tag{}, AllOrNone{}, std::true_type{}, std::true_type{});
+        else
+          tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{}, std::true_type{});
         pend_kb = ks + KT * 32;
       };
       static_assert(TPS == 2 || TPS == 4, "one stage is two or four key tiles");
@@ -518,10 +534,10 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
         constexpr int KT = decltype(kt_tag)::value;
         using par_tag = std::integral_constant<int, KT & 1>;
         if (st * TPS + KT < ntw) {
-          tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{});
+          tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{}, std::false_type{});
           pend_kb = ks + KT * 32;
         } else if (st * TPS + KT == ntw) {
-          tile(buf, 0, par_tag{}, PerElem{}, std::false_type{});
+          tile(buf, 0, par_tag{}, PerElem{}, std::false_type{}, std::false_type{});
           pend_kb = kNone;
         }
       };
@@ -539,7 +555,7 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   }
   if (!active) return;
   // with a whole number of stages the pending tile is the last (odd) one
-  if (ntw > 0 && ntw % TPS == 0) tile(smA, 0, P0{}, PerElem{}, std::false_type{});
+  if (ntw > 0 && ntw % TPS == 0) tile(smA, 0, P0{}, PerElem{}, std::false_type{}, std::false_type{});
 
   // merge the two half-waves (same query column, disjoint keys) and store
 #pragma unroll
