@@ -782,11 +782,8 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   };
   // a sub-tile in stage slot U that every row of which sees every key of the
   // wave: chain j of MFMAs with the terms of chain j-DIST in between
-  auto sub_tile = [&](const QTile2<ROWB> &cur, auto u_tag) __attribute__((always_inline)) {
+  auto sub_tile = [&](const QTile2<ROWB> &cur, auto u_tag, const frag (&av)[NS]) __attribute__((always_inline)) {
     constexpr int U = decltype(u_tag)::value;
-    frag av[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) av[s] = load_frag<frag>(cur.q + swz_off<T, D>(U * 32 + col, s * 2 * E + hi * E));
     // this sub-tile's LSE, read once the pending chains no longer need plv
     float clv[16];
 #pragma unroll
@@ -803,7 +800,7 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
           acc[j] = MM::run(av[s], kf[j][s], acc[j]);
           terms(pc, (s * 16) / NS, ((s + 1) * 16) / NS, prev ? plv : clv, ts);
         }
-        interleave_mfma_valu<NS, (48 / NS > 0 ? 48 / NS : 1)>();
+        interleave_mfma_valu<NS, (24 / NS > 0 ? 24 / NS : 1)>();
       } else {
 #pragma unroll
         for (int s = 0; s < NS; ++s) acc[j] = MM::run(av[s], kf[j][s], acc[j]);
@@ -832,12 +829,9 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
   // partial sums per chain, elements ascending) and a masked term is an
   // exact 0, so a key that sees every row of the sub-tile gets the same bits
   // on either path.
-  auto sub_masked = [&](const QTile2<ROWB> &cur, auto u_tag) __attribute__((always_inline)) {
+  auto sub_masked = [&](const QTile2<ROWB> &cur, auto u_tag, const frag (&av)[NS]) __attribute__((always_inline)) {
     constexpr int U = decltype(u_tag)::value;
     settle();
-    frag av[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) av[s] = load_frag<frag>(cur.q + swz_off<T, D>(U * 32 + col, s * 2 * E + hi * E));
 #pragma unroll
     for (int j = 0; j < NKT; ++j) {
       acc[j] = f32x16{};
@@ -880,10 +874,16 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
         constexpr int U = decltype(u_tag)::value;
         const int nv = min(32, r_hi - (rs + U * 32));  // valid rows of the sub-tile
         if (nv > 0) {
+          // the query fragments are read together with the positions that
+          // classify the sub-tile: one LDS round trip before the first MFMA
+          frag av[NS];
+#pragma unroll
+          for (int s = 0; s < NS; ++s)
+            av[s] = load_frag<frag>(cur.q + swz_off<T, D>(U * 32 + col, s * 2 * E + hi * E));
           const int qmin = cur.pos[U * 32], qmax = cur.pos[U * 32 + nv - 1];
           if (qmax >= kmin) {  // else no row of the sub-tile sees a key of the wave
-            if (qmin >= kmax) sub_tile(cur, u_tag);
-            else sub_masked(cur, u_tag);
+            if (qmin >= kmax) sub_tile(cur, u_tag, av);
+            else sub_masked(cur, u_tag, av);
           }
         }
       };
