@@ -763,11 +763,17 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
 #pragma unroll
   for (int e = 0; e < 16; ++e) plv[e] = INFINITY;
 
-  // exp2 terms of chain c (its accumulators in set c) for elements [e0, e1)
+  // exp2 terms of chain c (its accumulators in set c) for elements [e0, e1);
+  // the two partial sums start at elements 0 and 1 (the same bits as 0 +
+  // term, since no term is negative)
   auto terms = [&](int c, int e0, int e1, const float *lv, float (&ts)[2])
       __attribute__((always_inline)) {
 #pragma unroll
-    for (int e = e0; e < e1; ++e) ts[e & 1] += __builtin_amdgcn_exp2f(acc[c][e] * cl2e - lv[e]);
+    for (int e = e0; e < e1; ++e) {
+      const float v = __builtin_amdgcn_exp2f(acc[c][e] * cl2e - lv[e]);
+      if (e < 2) ts[e] = v;
+      else ts[e & 1] += v;
+    }
   };
   // the sub-tile's LSE of this lane's rows (log2 units)
   auto load_lv = [&](const QTile2<ROWB> &cur, int U, float (&lv)[16]) __attribute__((always_inline)) {
