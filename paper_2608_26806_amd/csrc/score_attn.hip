@@ -505,10 +505,8 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
         constexpr int KT = decltype(kt_tag)::value;
         using par_tag = std::integral_constant<int, KT & 1>;
         // a lane that sees only part of the pending tile needs the masked
-        // variant (this check also covers the latency of the tile's first
-        // LDS reads)
-        // the tile's first fragments are read before the check, whose VALU
-        // work then covers their latency
+        // variant; the tile's first fragments are read before this check,
+        // whose VALU work then covers their latency
 #pragma unroll
         for (int s = 0; s < PF; ++s)
           pf[s] = load_frag<frag>(buf + swz_off<T, D>(KT * 32 + col, s * 2 * E + hi * E));
