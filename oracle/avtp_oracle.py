@@ -428,3 +428,64 @@ def layer_select(A, k: int):
     rank_sum = ranks.sum(axis=1)
     order = sorted(range(L), key=lambda l: (int(rank_sum[l]), l))
     return rank_sum, rank_sum / float(N), sorted(order[:k])
+
+
+# ---------------------------------------------------------------------------
+# O6: progressive pruning across layers (Sec. 3.3.1, Sec. 3.3.2)
+# ---------------------------------------------------------------------------
+def pruned_layout(layout, keep_idx, cu_out, keep_total_next):
+    """The packed layout of the kept tokens, for the next pruning layer.
+
+    Pruning keeps a subsequence of every sequence (Method, "Visual Token
+    Pruning"), so the kept tokens of sequence b, in their original order,
+    become sequence b of the next layer: kept token r of the batch gets index
+    r.  An image keeps its kept tokens (its start is the new index of its
+    first kept token, or where it would be if it kept none); every text token
+    is kept.  keep_total_next is the next layer's keep totals (the schedule is
+    the caller's).  Returns an object with the layout's array attributes."""
+    from types import SimpleNamespace
+    keep_idx = np.asarray(keep_idx, dtype=np.int64)
+    cu_out = np.asarray(cu_out, dtype=np.int64)
+    cu_img = np.asarray(layout.cu_img, dtype=np.int64)
+    cu_text = np.asarray(layout.cu_text, dtype=np.int64)
+    img_start, img_len, text_pos = [], [], []
+    for b in range(len(cu_out) - 1):
+        kept = keep_idx[cu_out[b]:cu_out[b + 1]].tolist()
+        new_index = {j: int(cu_out[b]) + r for r, j in enumerate(kept)}
+        for i in range(cu_img[b], cu_img[b + 1]):
+            s0, n = int(layout.img_start[i]), int(layout.img_len[i])
+            img_start.append(int(cu_out[b]) + sum(1 for j in kept if j < s0))
+            img_len.append(sum(1 for j in kept if s0 <= j < s0 + n))
+        for t in range(cu_text[b], cu_text[b + 1]):
+            text_pos.append(new_index[int(layout.text_pos[t])])
+    a = lambda v: np.asarray(v, dtype=np.int32)
+    return SimpleNamespace(cu_seqlens=a(cu_out), img_start=a(img_start), img_len=a(img_len),
+                           cu_img=a(cu_img), text_pos=a(text_pos), cu_text=a(cu_text),
+                           keep_total=a(keep_total_next), B=len(cu_out) - 1,
+                           n_img=len(img_len), N_tok=int(cu_out[-1]), T_tot=len(text_pos))
+
+
+def keep_totals(layout, keep_pct: int):
+    """keep_total[b] = round-half-up(keep_pct % of sequence b's visual tokens)."""
+    cu = np.asarray(layout.cu_img, dtype=np.int64)
+    n = np.asarray(layout.img_len, dtype=np.int64)
+    return np.array([(keep_pct * int(n[cu[b]:cu[b + 1]].sum()) + 50) // 100
+                     for b in range(len(cu) - 1)], dtype=np.int32)
+
+
+def progressive_step(layout, h_cur, h_prior, dtype: str, keep_pct_next: int, alpha: float = 1.0,
+                     lo_permille: int = 50, hi_permille: int = 950, floor_abs: int = 0):
+    """One pruning layer of the progressive schedule in VARIATION mode: the
+    importance of each visual token against its embedding after the previous
+    pruning (h_prior, Sec. 3.3.1), per-image budgets, per-image top-k, and the
+    kept tokens' hidden states, which are both this layer's output and the
+    next pruning layer's h_prior.  Returns (next layout, kept h_cur, keep_idx,
+    budgets, scores)."""
+    s, isum = variation_scores(layout, h_cur, h_prior, dtype)
+    bud = budget(layout, np.asarray(isum, dtype=np.float32), alpha, lo_permille, hi_permille,
+                 floor_abs)
+    keep, cu_out = select(layout, np.asarray(s, dtype=np.float32), bud)
+    h_next = compact(keep, h_cur)
+    nxt = pruned_layout(layout, keep, cu_out, np.zeros(len(cu_out) - 1, dtype=np.int32))
+    nxt.keep_total = keep_totals(nxt, keep_pct_next)
+    return nxt, h_next, keep, bud, s
