@@ -101,6 +101,54 @@ def time_layer_selection(dl, isum, stream, dev, reps: int = 50) -> dict:
     return res
 
 
+def time_variation_and_progressive(dl, lay, hid, keep, cu_out, stream, dev, reps: int = 20) -> dict:
+    """The VARIATION score (Sec. 3.3.1, row a4) on this workload's hidden states
+    with a synthetic h_prior (h + 0.1 N(0,1), seeded), against the HBM roofline
+    (2 x hidden x element bytes per visual token); the next-layer layout
+    update; and one whole progressive pruning step (score, budget, select,
+    compaction of the hidden states, layout update, and the host copy of the
+    new layout's index arrays)."""
+    import torch
+
+    from paper_2608_26806_amd import avtp as A
+    from paper_2608_26806_amd.progressive import ProgressivePruner
+
+    g = torch.Generator(device=dev)
+    g.manual_seed(3311)
+    h_prior = (hid.float() + 0.1 * torch.randn(hid.shape, generator=g, device=dev)).to(hid.dtype)
+    M = int(lay.img_len.sum())
+    alg = 2.0 * M * hid.shape[1] * hid.element_size()
+    sc = torch.empty(lay.N_tok, dtype=torch.float32, device=dev)
+    isum = torch.empty(max(1, lay.n_img), dtype=torch.float32, device=dev)
+
+    def timed(fn):
+        fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+        for r in range(reps):
+            ev[2 * r].record(stream)
+            fn()
+            ev[2 * r + 1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.median([ev[2 * r].elapsed_time(ev[2 * r + 1]) for r in range(reps)])) * 1e3
+
+    t_var = timed(lambda: A.score_variation(dl, hid, h_prior, scores=sc, img_sum=isum))
+    t_lay = timed(lambda: A.pruned_layout(dl, keep, cu_out))
+    steps = []
+    for _ in range(3):
+        pr = ProgressivePruner(dl, h_prior)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pr.step(hid, keep_pct_next=50)
+        torch.cuda.synchronize()
+        steps.append((time.perf_counter() - t0) * 1e6)
+    gbs = alg / (t_var * 1e-6) / 1e9
+    return {"variation_score": {"kernel": "variation_kernel (+ finalize)", "bound": "hbm",
+                                "us": t_var, "alg_bytes": alg, "achieved": gbs,
+                                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS},
+            "pruned_layout_us": t_lay,
+            "progressive_step_us_wall": float(np.median(steps))}
+
+
 def algorithmic_counts(lay, Hq, d, row_bytes_total):
     """Per-launch algorithmic work of each stage.
 
@@ -266,6 +314,7 @@ def main():
         print(f"warning: device status flags {st.tolist()}", file=sys.stderr)
 
     layer_sel = time_layer_selection(dl, isum, stream, dev)
+    var_prog = time_variation_and_progressive(dl, lay, hid, keep, cu_out, stream, dev)
 
     M = int(lay.img_len.sum())
     ms_layer = float(np.median(layer_ms))
@@ -320,6 +369,7 @@ def main():
                              "alg_bytes": comp_bytes},
         "select_plus_compact_hbm_frac": selcomp_gbs / PEAK_HBM_GBS,
         "layer_selection": layer_sel,
+        "variation_and_progressive": var_prog,
         "wall_s_timed_region": wall,
         "input_generation_s": gen_s,
     }

@@ -201,6 +201,29 @@ int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t 
                  int64_t n_out, const avtp_tensor *tensors, int n_tensors);
 
 /* ------------------------------------------------------------------------
+ * avtp_pruned_layout -- the layout of the kept tokens, for the next pruning
+ * layer of a progressive schedule (Sec. 3.3.2: pruning at several selected
+ * layers; Sec. 3.3.1: the next layer's h^prior is the hidden state after this
+ * pruning, i.e. this layer's compacted hidden rows).  Pruning keeps a
+ * subsequence of every sequence (Method, "Visual Token Pruning"): kept token
+ * r of the batch (keep_idx[r], from avtp_select, ascending per sequence)
+ * becomes token r of the next layer.  Writes, as device int32 arrays of the
+ * next layer's avtp_layout:
+ *   cu_seqlens_out [B+1] = cu_out;
+ *   img_start_out, img_len_out [n_img]: image i's first new index and its
+ *     number of kept tokens (an image that keeps none has length 0 and sits
+ *     where its tokens were);
+ *   text_pos_out [T_tot]: the new index of every text token (all are kept);
+ *   cu_img_out, cu_text_out [B+1]: unchanged copies.
+ * The next layer's keep totals (the schedule) are the caller's.  Host
+ * mirrors of the next layout are the caller's copies of these arrays.
+ * ---------------------------------------------------------------------- */
+int avtp_pruned_layout(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,
+                       const int32_t *cu_out, int32_t *cu_seqlens_out, int32_t *img_start_out,
+                       int32_t *img_len_out, int32_t *cu_img_out, int32_t *text_pos_out,
+                       int32_t *cu_text_out);
+
+/* ------------------------------------------------------------------------
  * Architecture-aware pruning-layer selection (Sec. 3.3.2), computed from
  * calibration prefills.  For sample i and layer l the paper sums the
  * attention the layer pays to every visual token,

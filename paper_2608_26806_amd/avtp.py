@@ -72,13 +72,14 @@ def lib() -> ctypes.CDLL:
         L.avtp_budget.argtypes = [vp, LP, vp, c_int, c_float, c_int, c_int, c_int, vp, vp]
         L.avtp_select.argtypes = [vp, LP, vp, vp, vp, ctypes.c_int64, vp, vp]
         L.avtp_compact.argtypes = [vp, LP, vp, ctypes.c_int64, ctypes.POINTER(_Tensor), c_int]
+        L.avtp_pruned_layout.argtypes = [vp, LP, vp, vp, vp, vp, vp, vp, vp, vp]
         L.avtp_layer_attention.argtypes = [vp, LP, vp, vp]
         L.avtp_layer_select.argtypes = [vp, vp, c_int, c_int, c_int, vp, vp]
         L.avtp_status_string.argtypes = [c_int]
         L.avtp_status_string.restype = ctypes.c_char_p
         L.avtp_version.restype = c_int
         for f in ("avtp_score", "avtp_row_lse", "avtp_budget", "avtp_select", "avtp_compact",
-                  "avtp_layer_attention", "avtp_layer_select"):
+                  "avtp_layer_attention", "avtp_layer_select", "avtp_pruned_layout"):
             getattr(L, f).restype = c_int
         _lib = L
     return _lib
@@ -292,6 +293,23 @@ def compact_new(dl: DeviceLayout, keep_idx: torch.Tensor, srcs: Sequence, stream
         pairs.append((src, dst, tdim))
     compact(dl, keep_idx, pairs, stream=stream)
     return outs
+
+
+# --------------------------------------------------------------------------- progressive pruning
+def pruned_layout(dl: DeviceLayout, keep_idx: torch.Tensor, cu_out: torch.Tensor,
+                  stream=None) -> dict:
+    """Device arrays of the next pruning layer's layout (all but keep_total)."""
+    dev = cu_out.device
+    out = {n: torch.empty(max(1, m), dtype=torch.int32, device=dev)
+           for n, m in (("cu_seqlens", dl.B + 1), ("img_start", dl.n_img), ("img_len", dl.n_img),
+                        ("cu_img", dl.B + 1), ("text_pos", dl.T_tot), ("cu_text", dl.B + 1))}
+    _check(lib().avtp_pruned_layout(_stream(stream), dl.ref(), _ptr(keep_idx), _ptr(cu_out),
+                                    *[_ptr(out[n]) for n in ("cu_seqlens", "img_start", "img_len",
+                                                             "cu_img", "text_pos", "cu_text")]),
+           "avtp_pruned_layout")
+    lens = {"cu_seqlens": dl.B + 1, "img_start": dl.n_img, "img_len": dl.n_img,
+            "cu_img": dl.B + 1, "text_pos": dl.T_tot, "cu_text": dl.B + 1}
+    return {n: t[: lens[n]] for n, t in out.items()}
 
 
 # --------------------------------------------------------------------------- layer selection

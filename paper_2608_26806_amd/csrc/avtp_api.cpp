@@ -216,6 +216,22 @@ int avtp_select(avtp_stream_t stream, const avtp_layout *layout, const float *sc
                                   keep_capacity, cu_out, status));
 }
 
+int avtp_pruned_layout(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,
+                       const int32_t *cu_out, int32_t *cu_seqlens_out, int32_t *img_start_out,
+                       int32_t *img_len_out, int32_t *cu_img_out, int32_t *text_pos_out,
+                       int32_t *cu_text_out) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  if (!cu_out || !cu_seqlens_out || !cu_img_out || !cu_text_out) return AVTP_ERR_INVALID_ARG;
+  if (L.n_img > 0 && (!img_start_out || !img_len_out)) return AVTP_ERR_INVALID_ARG;
+  if (L.T_tot > 0 && !text_pos_out) return AVTP_ERR_INVALID_ARG;
+  if (n_out_of(layout) > 0 && !keep_idx) return AVTP_ERR_INVALID_ARG;
+  return hip_status(launch_pruned_layout((hipStream_t)stream, L, keep_idx, cu_out, cu_seqlens_out,
+                                         img_start_out, img_len_out, cu_img_out, text_pos_out,
+                                         cu_text_out));
+}
+
 int avtp_layer_attention(avtp_stream_t stream, const avtp_layout *layout, const float *img_sum,
                          float *A_out) {
   DevLayout L;

@@ -64,6 +64,12 @@ hipError_t launch_select(hipStream_t stream, const DevLayout &L, const float *sc
 hipError_t launch_compact(hipStream_t stream, const DevLayout &L, const int32_t *keep_idx,
                           int64_t n_out, const avtp_tensor *tensors, int n_tensors);
 
+// Layout of the kept tokens for the next pruning layer.
+hipError_t launch_pruned_layout(hipStream_t stream, const DevLayout &L, const int32_t *keep_idx,
+                                const int32_t *cu_out, int32_t *cu_seqlens_out,
+                                int32_t *img_start_out, int32_t *img_len_out, int32_t *cu_img_out,
+                                int32_t *text_pos_out, int32_t *cu_text_out);
+
 // Pruning-layer selection (Sec. 3.3.2): per-sample attention of one layer,
 // and the per-sample ranks, their sums and the top-k layers.
 hipError_t launch_layer_attention(hipStream_t stream, const DevLayout &L, const float *img_sum,

@@ -150,3 +150,15 @@ def test_layer_selection_arguments_rejected_on_host():
     assert lib.avtp_layer_select(None, p, 4, 3, 0, p, p) == A.ERR_INVALID_ARG      # k = 0
     assert lib.avtp_layer_attention(None, None, p, p) == A.ERR_INVALID_ARG         # no layout
     assert lib.avtp_layer_attention(None, _dl().ref(), p, None) == A.ERR_INVALID_ARG
+
+
+def test_pruned_layout_arguments_rejected_on_host():
+    lib = A.lib()
+    buf = torch.zeros(256, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    dl = _dl()
+    assert lib.avtp_pruned_layout(None, None, p, p, p, p, p, p, p, p) == A.ERR_INVALID_ARG
+    assert lib.avtp_pruned_layout(None, dl.ref(), p, None, p, p, p, p, p, p) == A.ERR_INVALID_ARG
+    assert lib.avtp_pruned_layout(None, dl.ref(), None, p, p, p, p, p, p, p) == A.ERR_INVALID_ARG
+    assert lib.avtp_pruned_layout(None, dl.ref(), p, p, p, None, p, p, p, p) == A.ERR_INVALID_ARG
+    assert lib.avtp_pruned_layout(None, dl.ref(), p, p, p, p, p, p, None, p) == A.ERR_INVALID_ARG
