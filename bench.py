@@ -149,6 +149,26 @@ def time_variation_and_progressive(dl, lay, hid, keep, cu_out, stream, dev, reps
             "progressive_step_us_wall": float(np.median(steps))}
 
 
+def time_select_compact(dl, scores, bud, pairs, stream, reps: int = 20) -> float:
+    """Median time of the fused selection + compaction (one launch) on this
+    step's scores, budgets and tensors."""
+    import torch
+
+    from paper_2608_26806_amd import avtp as A
+
+    def once():
+        A.select_compact(dl, scores, bud, pairs)
+
+    once()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+    for r in range(reps):
+        ev[2 * r].record(stream)
+        once()
+        ev[2 * r + 1].record(stream)
+    torch.cuda.synchronize()
+    return float(np.median([ev[2 * r].elapsed_time(ev[2 * r + 1]) for r in range(reps)])) * 1e3
+
+
 def algorithmic_counts(lay, Hq, d, row_bytes_total):
     """Per-launch algorithmic work of each stage.
 
@@ -315,6 +335,7 @@ def main():
 
     layer_sel = time_layer_selection(dl, isum, stream, dev)
     var_prog = time_variation_and_progressive(dl, lay, hid, keep, cu_out, stream, dev)
+    fused_us = time_select_compact(dl, scores, bud, pairs, stream)
 
     M = int(lay.img_len.sum())
     ms_layer = float(np.median(layer_ms))
@@ -368,6 +389,10 @@ def main():
                              "unit": "GB/s", "frac": comp_gbs / PEAK_HBM_GBS,
                              "alg_bytes": comp_bytes},
         "select_plus_compact_hbm_frac": selcomp_gbs / PEAK_HBM_GBS,
+        "select_compact_fused": {
+            "us": fused_us,
+            "hbm_frac": (comp_bytes + sel_bytes) / (fused_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+            "separate_calls_us": (ms["select"] + ms["compact"]) * 1e3},
         "layer_selection": layer_sel,
         "variation_and_progressive": var_prog,
         "wall_s_timed_region": wall,

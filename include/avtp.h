@@ -256,6 +256,20 @@ int avtp_layer_attention(avtp_stream_t stream, const avtp_layout *layout, const 
 int avtp_layer_select(avtp_stream_t stream, const float *A, int L, int N, int k,
                       int32_t *rank_sum, int32_t *selected);
 
+/* ------------------------------------------------------------------------
+ * avtp_select_compact -- avtp_select followed by avtp_compact of the same
+ * tensors to n_out = T_tot + sum(keep_total) rows, in one launch (for the
+ * small configurations, where the launches and the selection's latency
+ * dominate).  Same arguments and outputs as the two calls; the kept rows and
+ * keep_idx are bit-identical to theirs.  Every image is handled by several
+ * blocks that each redo its selection and copy an interleaved share of its
+ * output rows, so no block waits for another.
+ * ---------------------------------------------------------------------- */
+int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const float *scores,
+                        const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
+                        int32_t *cu_out, int32_t *status, const avtp_tensor *tensors,
+                        int n_tensors);
+
 /* Human-readable name of an avtp_status value (static string). */
 const char *avtp_status_string(int status);
 

@@ -73,13 +73,16 @@ def lib() -> ctypes.CDLL:
         L.avtp_select.argtypes = [vp, LP, vp, vp, vp, ctypes.c_int64, vp, vp]
         L.avtp_compact.argtypes = [vp, LP, vp, ctypes.c_int64, ctypes.POINTER(_Tensor), c_int]
         L.avtp_pruned_layout.argtypes = [vp, LP, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.avtp_select_compact.argtypes = [vp, LP, vp, vp, vp, ctypes.c_int64, vp, vp,
+                                          ctypes.POINTER(_Tensor), c_int]
         L.avtp_layer_attention.argtypes = [vp, LP, vp, vp]
         L.avtp_layer_select.argtypes = [vp, vp, c_int, c_int, c_int, vp, vp]
         L.avtp_status_string.argtypes = [c_int]
         L.avtp_status_string.restype = ctypes.c_char_p
         L.avtp_version.restype = c_int
         for f in ("avtp_score", "avtp_row_lse", "avtp_budget", "avtp_select", "avtp_compact",
-                  "avtp_layer_attention", "avtp_layer_select", "avtp_pruned_layout"):
+                  "avtp_layer_attention", "avtp_layer_select", "avtp_pruned_layout",
+                  "avtp_select_compact"):
             getattr(L, f).restype = c_int
         _lib = L
     return _lib
@@ -280,6 +283,23 @@ def compact(dl: DeviceLayout, keep_idx: torch.Tensor, pairs: Sequence, n_out: Op
     n = dl.N_out if n_out is None else int(n_out)
     _check(lib().avtp_compact(_stream(stream), dl.ref(), _ptr(keep_idx), n, arr, len(descs)),
            "avtp_compact")
+
+
+def select_compact(dl: DeviceLayout, scores: torch.Tensor, budget_: torch.Tensor, pairs: Sequence,
+                   keep_idx: Optional[torch.Tensor] = None, cu_out: Optional[torch.Tensor] = None,
+                   status: Optional[torch.Tensor] = None, stream=None):
+    """avtp_select and avtp_compact in one launch; pairs as for compact."""
+    dev = scores.device
+    if keep_idx is None:
+        keep_idx = torch.empty(max(1, dl.N_out), dtype=torch.int32, device=dev)
+    if cu_out is None:
+        cu_out = torch.empty(dl.B + 1, dtype=torch.int32, device=dev)
+    descs = [tensor_desc(p[0], p[1], p[2] if len(p) > 2 else 0) for p in pairs]
+    arr = (_Tensor * max(1, len(descs)))(*descs)
+    _check(lib().avtp_select_compact(_stream(stream), dl.ref(), _ptr(scores), _ptr(budget_),
+                                     _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out), _ptr(status),
+                                     arr, len(descs)), "avtp_select_compact")
+    return keep_idx[: dl.N_out], cu_out
 
 
 def compact_new(dl: DeviceLayout, keep_idx: torch.Tensor, srcs: Sequence, stream=None):

@@ -249,16 +249,12 @@ int avtp_layer_select(avtp_stream_t stream, const float *A, int L, int N, int k,
   return hip_status(launch_layer_select((hipStream_t)stream, A, L, N, k, rank_sum, selected));
 }
 
-int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,
-                 int64_t n_out, const avtp_tensor *tensors, int n_tensors) {
-  DevLayout L;
-  int rc = check_layout(layout, &L);
-  if (rc != AVTP_OK) return rc;
+// tensor descriptors of a compaction to n_out rows
+static int check_tensors(const DevLayout &L, int64_t n_out, const avtp_tensor *tensors,
+                         int n_tensors) {
   if (n_tensors < 0 || n_out < 0) return AVTP_ERR_INVALID_ARG;
   if (n_tensors > AVTP_MAX_TENSORS) return AVTP_ERR_UNSUPPORTED;
   if (n_tensors > 0 && !tensors) return AVTP_ERR_INVALID_ARG;
-  if (n_out > 0 && !keep_idx) return AVTP_ERR_INVALID_ARG;
-  if (n_out > n_out_of(layout)) return AVTP_ERR_INVALID_ARG;
   for (int i = 0; i < n_tensors; ++i) {
     const avtp_tensor &t = tensors[i];
     if (!t.src || !t.dst || t.row_bytes < 1 || t.planes < 1) return AVTP_ERR_INVALID_ARG;
@@ -267,8 +263,36 @@ int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t 
                          t.dst_plane_stride < n_out * t.dst_stride))
       return AVTP_ERR_INVALID_ARG;
   }
+  return AVTP_OK;
+}
+
+int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,
+                 int64_t n_out, const avtp_tensor *tensors, int n_tensors) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  rc = check_tensors(L, n_out, tensors, n_tensors);
+  if (rc != AVTP_OK) return rc;
+  if (n_out > 0 && !keep_idx) return AVTP_ERR_INVALID_ARG;
+  if (n_out > n_out_of(layout)) return AVTP_ERR_INVALID_ARG;
   if (n_out == 0 || n_tensors == 0) return AVTP_OK;
   return hip_status(launch_compact((hipStream_t)stream, L, keep_idx, n_out, tensors, n_tensors));
+}
+
+int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const float *scores,
+                        const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
+                        int32_t *cu_out, int32_t *status, const avtp_tensor *tensors,
+                        int n_tensors) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  if (!scores || !cu_out || (L.n_img > 0 && !budget)) return AVTP_ERR_INVALID_ARG;
+  const int64_t need = n_out_of(layout);
+  if (keep_capacity < need || (need > 0 && !keep_idx)) return AVTP_ERR_INVALID_ARG;
+  rc = check_tensors(L, need, tensors, n_tensors);
+  if (rc != AVTP_OK) return rc;
+  return hip_status(launch_select_compact((hipStream_t)stream, L, scores, budget, keep_idx,
+                                          keep_capacity, cu_out, status, need, tensors, n_tensors));
 }
 
 }  // extern "C"

@@ -63,6 +63,11 @@ hipError_t launch_select(hipStream_t stream, const DevLayout &L, const float *sc
                          int32_t *cu_out, int32_t *status);
 hipError_t launch_compact(hipStream_t stream, const DevLayout &L, const int32_t *keep_idx,
                           int64_t n_out, const avtp_tensor *tensors, int n_tensors);
+// avtp_select and avtp_compact (to the n_out of the layout) in one launch.
+hipError_t launch_select_compact(hipStream_t stream, const DevLayout &L, const float *scores,
+                                 const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
+                                 int32_t *cu_out, int32_t *status, int64_t n_out,
+                                 const avtp_tensor *tensors, int n_tensors);
 
 // Layout of the kept tokens for the next pruning layer.
 hipError_t launch_pruned_layout(hipStream_t stream, const DevLayout &L, const int32_t *keep_idx,

@@ -12,25 +12,13 @@
 #include <stdint.h>
 
 #include "avtp_internal.h"
+#include "row_copy.h"
 
 namespace avtp {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kBlockBytes = 32768;  // target bytes per block
-
-struct CTensor {
-  const char *src;
-  char *dst;
-  long long src_stride, dst_stride, src_plane_stride, dst_plane_stride;
-  int units;       // vector units per row
-  int vshift;      // log2 of the vector width in bytes
-  int lpr_shift;   // log2 of lanes per row
-  int planes;
-  int rows_per_block;
-  int blocks_per_plane;
-  int block_begin;
-};
 
 struct CArgs {
   CTensor t[AVTP_MAX_TENSORS];
@@ -47,20 +35,10 @@ __device__ inline void copy_rows(const CTensor &T, const int32_t *__restrict__ k
   const int lpr = 1 << T.lpr_shift;
   const int lane = tid & (lpr - 1);
   const int rows_per_pass = kThreads >> T.lpr_shift;
-  const char *src = T.src + plane * T.src_plane_stride;
-  char *dst = T.dst + plane * T.dst_plane_stride;
   for (long long r = r0 + (tid >> T.lpr_shift); r < r1; r += rows_per_pass) {
     const int j = keep_idx[r];
     if ((unsigned)j >= (unsigned)N_tok) continue;  // out-of-range index: row left untouched
-    const V *s = reinterpret_cast<const V *>(src + (long long)j * T.src_stride);
-    V *d = reinterpret_cast<V *>(dst + r * T.dst_stride);
-    int u = lane;
-    for (; u + lpr < T.units; u += 2 * lpr) {  // two independent loads in flight
-      const V a = s[u], b = s[u + lpr];
-      d[u] = a;
-      d[u + lpr] = b;
-    }
-    if (u < T.units) d[u] = s[u];
+    copy_one_row<V>(T, plane, j, r, lane);
   }
 }
 
@@ -83,12 +61,6 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CArgs a) {
   }
 }
 
-int ilog2(long long v) {
-  int s = 0;
-  while ((1ll << (s + 1)) <= v) ++s;
-  return s;
-}
-
 }  // namespace
 
 hipError_t launch_compact(hipStream_t st, const DevLayout &L, const int32_t *keep_idx,
@@ -101,25 +73,9 @@ hipError_t launch_compact(hipStream_t st, const DevLayout &L, const int32_t *kee
   long long blocks = 0;
   for (int i = 0; i < n_tensors; ++i) {
     const avtp_tensor &x = tensors[i];
-    long long v = 16;
-    auto misaligned = [&](long long m) {
-      return (x.row_bytes % m) || (x.src_stride % m) || (x.dst_stride % m) ||
-             ((uintptr_t)x.src % m) || ((uintptr_t)x.dst % m) ||
-             (x.planes > 1 && ((x.src_plane_stride % m) || (x.dst_plane_stride % m)));
-    };
-    while (v > 1 && misaligned(v)) v >>= 1;
     CTensor &T = a.t[i];
-    T.src = (const char *)x.src;
-    T.dst = (char *)x.dst;
-    T.src_stride = x.src_stride;
-    T.dst_stride = x.dst_stride;
-    T.src_plane_stride = x.src_plane_stride;
-    T.dst_plane_stride = x.dst_plane_stride;
-    T.vshift = ilog2(v);
-    T.units = (int)(x.row_bytes / v);
-    long long lpr = 1;
-    while (lpr < T.units && lpr < kThreads) lpr <<= 1;
-    T.lpr_shift = ilog2(lpr);
+    describe_tensor(x, kThreads, T);
+    const long long lpr = 1ll << T.lpr_shift;
     const long long rows_per_pass = kThreads / lpr;
     long long rpb = (kBlockBytes + x.row_bytes - 1) / x.row_bytes;
     rpb = ((rpb + rows_per_pass - 1) / rows_per_pass) * rows_per_pass;

@@ -16,6 +16,7 @@
 #include <stdint.h>
 
 #include "avtp_internal.h"
+#include "row_copy.h"
 
 namespace avtp {
 namespace {
@@ -116,13 +117,17 @@ __device__ inline void pick_digit(const uint32_t *hist, int krem, uint32_t *sh_d
 // output follows the same budget prefix, and the matching cu_out entries.
 // A text row t goes to  t + (budgets of the images before it);  an image's
 // kept tokens start at  (first text row after it) + (budgets before it).
-__global__ __launch_bounds__(kThreads) void select_kernel(
-    const float *__restrict__ scores, const int32_t *__restrict__ budget,
-    const int32_t *__restrict__ img_start, const int32_t *__restrict__ img_len,
-    const int32_t *__restrict__ cu_img, const int32_t *__restrict__ cu_text,
-    const int32_t *__restrict__ text_pos, int B, int n_img, int T_tot,
-    int32_t *__restrict__ keep_idx, long long cap, int32_t *__restrict__ cu_out,
-    int32_t *__restrict__ status) {
+struct SelArgs {
+  const float *scores;
+  const int32_t *budget, *img_start, *img_len, *cu_img, *cu_text, *text_pos;
+  int B, n_img, T_tot;
+  int32_t *cu_out;  // null: not written (all but one slice of the fused kernel)
+};
+
+// The kept tokens of image i (and the text rows around it), reported as
+// put(output index, token index, sequence) in no particular order.
+template <typename Put>
+__device__ __attribute__((always_inline)) inline void select_image(const SelArgs &A, int i, Put put) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t keys[kLdsKeys];
   __shared__ int wsum[4];
@@ -130,19 +135,23 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
   __shared__ uint32_t sh_digit;
   __shared__ int sh_krem, sh_b;
   const int tid = threadIdx.x;
-
-  auto put = [&](long long o, int32_t v, int seq) __attribute__((always_inline)) {
-    if (o < cap) keep_idx[o] = v;
-    else if (status) atomicOr(status + seq, AVTP_FLAG_OUT_CAPACITY);
-  };
+  const float *__restrict__ scores = A.scores;
+  const int32_t *__restrict__ budget = A.budget;
+  const int32_t *__restrict__ img_start = A.img_start;
+  const int32_t *__restrict__ img_len = A.img_len;
+  const int32_t *__restrict__ cu_img = A.cu_img;
+  const int32_t *__restrict__ cu_text = A.cu_text;
+  const int32_t *__restrict__ text_pos = A.text_pos;
+  const int B = A.B, n_img = A.n_img, T_tot = A.T_tot;
+  int32_t *__restrict__ cu_out = A.cu_out;
 
   if (n_img == 0) {  // no images at all: every text row is kept in place
     for (int t = tid; t < T_tot; t += kThreads) put(t, text_pos[t], 0);
-    for (int c = tid; c <= B; c += kThreads) cu_out[c] = cu_text[c];
+    if (cu_out)
+      for (int c = tid; c <= B; c += kThreads) cu_out[c] = cu_text[c];
     return;
   }
 
-  const int i = blockIdx.x;
   for (int c = tid; c < B; c += kThreads)  // the sequence holding image i
     if (cu_img[c] <= i && i < cu_img[c + 1]) sh_b = c;
   const int st = img_start[i], n = img_len[i];
@@ -176,8 +185,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int ci = cu_img[c];
     const bool empty_before = c < B && ci == i && cu_img[c + 1] == i;  // image-less, before i
     const bool empty_after = last && i == n_img - 1 && ci == n_img;    // trailing ones and B
-    if ((first && c == b) || empty_before) cu_out[c] = (int32_t)(cu_text[c] + pre);
-    if (empty_after) cu_out[c] = (int32_t)(cu_text[c] + pre + k);
+    if (cu_out && ((first && c == b) || empty_before)) cu_out[c] = (int32_t)(cu_text[c] + pre);
+    if (cu_out && empty_after) cu_out[c] = (int32_t)(cu_text[c] + pre + k);
     if (empty_before || (empty_after && c < B)) {
       const long long add = empty_before ? pre : pre + k;
       for (int t = cu_text[c]; t < cu_text[c + 1]; ++t) put(t + add, text_pos[t], c);
@@ -257,15 +266,122 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
   }
 }
 
+__global__ __launch_bounds__(kThreads) void select_kernel(SelArgs A, int32_t *__restrict__ keep_idx,
+                                                         long long cap, int32_t *__restrict__ status) {
+  select_image(A, A.n_img > 0 ? (int)blockIdx.x : 0,
+               [&](long long o, int32_t v, int seq) __attribute__((always_inline)) {
+                 if (o < cap) keep_idx[o] = v;
+                 else if (status) atomicOr(status + seq, AVTP_FLAG_OUT_CAPACITY);
+               });
+}
+
+// Fused selection and compaction: S blocks per image (slices).  Every slice
+// runs the image's selection (its keys are few and sit in LDS), owns the
+// output rows o with o mod S == slice, writes their keep_idx entries, lists
+// them in LDS, and then copies those rows of every tensor with groups of
+// lanes.  No block waits for another.
+constexpr int kListCap = 4096;  // output rows one slice may own (the host sizes S for it)
+
+struct SCArgs {
+  SelArgs sel;
+  int32_t *keep_idx;
+  long long cap;    // keep_idx entries
+  long long n_out;  // rows of every destination tensor (rows at or past it are not copied)
+  int32_t *status;
+  int S;
+  int n_t;
+  CTensor t[AVTP_MAX_TENSORS];
+};
+
+// The listed rows of one tensor, a power-of-two group of lanes per row (as in
+// the compaction kernel).
+template <typename V>
+__device__ inline void copy_listed(const CTensor &T, const int *lo, const int *lj, int n) {
+  const int lpr_shift = T.lpr_shift;
+  const int lane = threadIdx.x & ((1 << lpr_shift) - 1);
+  const int per_pass = kThreads >> lpr_shift;
+  for (int p = 0; p < T.planes; ++p)
+    for (int e = (int)(threadIdx.x >> lpr_shift); e < n; e += per_pass)
+      copy_one_row<V>(T, p, lj[e], lo[e], lane);
+}
+
+__global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a) {
+  __shared__ int list_o[kListCap], list_j[kListCap];
+  __shared__ int list_n;
+  const int S = a.S;
+  const int img = (int)blockIdx.x / S, sl = (int)blockIdx.x - img * S;
+  if (threadIdx.x == 0) list_n = 0;
+  __syncthreads();
+  SelArgs A = a.sel;
+  if (sl != 0) A.cu_out = nullptr;
+  select_image(A, img, [&](long long o, int32_t v, int seq) __attribute__((always_inline)) {
+    if ((int)(o % S) != sl) return;
+    if (o >= a.cap) {
+      if (a.status) atomicOr(a.status + seq, AVTP_FLAG_OUT_CAPACITY);
+      return;
+    }
+    a.keep_idx[o] = v;
+    if (o >= a.n_out) return;
+    const int e = atomicAdd(&list_n, 1);
+    if (e < kListCap) {
+      list_o[e] = (int)o;
+      list_j[e] = v;
+    } else if (a.status) {  // (the host sizes S so that this does not happen)
+      atomicOr(a.status + seq, AVTP_FLAG_OUT_CAPACITY);
+    }
+  });
+  __syncthreads();
+  const int n = min(list_n, kListCap);
+  for (int ti = 0; ti < a.n_t; ++ti) {
+    const CTensor &T = a.t[ti];
+    switch (T.vshift) {
+      case 4: copy_listed<uint4>(T, list_o, list_j, n); break;
+      case 3: copy_listed<uint2>(T, list_o, list_j, n); break;
+      case 2: copy_listed<uint32_t>(T, list_o, list_j, n); break;
+      case 1: copy_listed<uint16_t>(T, list_o, list_j, n); break;
+      default: copy_listed<uint8_t>(T, list_o, list_j, n); break;
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_select_compact(hipStream_t st, const DevLayout &L, const float *scores,
+                                 const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
+                                 int32_t *cu_out, int32_t *status, int64_t n_out,
+                                 const avtp_tensor *tensors, int n_tensors) {
+  SCArgs a;
+  a.sel = SelArgs{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
+                  L.B, L.n_img, L.T_tot, cu_out};
+  a.keep_idx = keep_idx;
+  a.cap = (long long)keep_capacity;
+  a.n_out = n_out;
+  a.status = status;
+  a.n_t = n_tensors;
+  for (int i = 0; i < n_tensors; ++i) describe_tensor(tensors[i], kThreads, a.t[i]);
+  // slices per image: about 1024 blocks in all, and few enough rows per
+  // slice for its list (an image block writes at most the image's tokens
+  // plus every text row; each contiguous run adds at most one to a share)
+  const long long bound = (long long)L.max_img_len + L.T_tot + 64;
+  const int images = L.n_img > 0 ? L.n_img : 1;
+  long long S = (1024 + images - 1) / images;
+  if (S > 64) S = 64;
+  const long long need = (bound + (kListCap - 64) - 1) / (kListCap - 64);
+  if (S < need) S = need;
+  if (S < 1) S = 1;
+  a.S = (int)S;
+  hipLaunchKernelGGL(select_compact_kernel, dim3((unsigned)(images * S)), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_select(hipStream_t st, const DevLayout &L, const float *scores,
                          const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
                          int32_t *cu_out, int32_t *status) {
   const int grid = L.n_img > 0 ? L.n_img : 1;
-  hipLaunchKernelGGL(select_kernel, dim3(grid), dim3(kThreads), 0, st, scores, budget, L.img_start,
-                     L.img_len, L.cu_img, L.cu_text, L.text_pos, L.B, L.n_img, L.T_tot, keep_idx,
-                     (long long)keep_capacity, cu_out, status);
+  const SelArgs A{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
+                  L.B, L.n_img, L.T_tot, cu_out};
+  hipLaunchKernelGGL(select_kernel, dim3(grid), dim3(kThreads), 0, st, A, keep_idx,
+                     (long long)keep_capacity, status);
   return hipGetLastError();
 }
 

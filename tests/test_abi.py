@@ -162,3 +162,16 @@ def test_pruned_layout_arguments_rejected_on_host():
     assert lib.avtp_pruned_layout(None, dl.ref(), None, p, p, p, p, p, p, p) == A.ERR_INVALID_ARG
     assert lib.avtp_pruned_layout(None, dl.ref(), p, p, p, None, p, p, p, p) == A.ERR_INVALID_ARG
     assert lib.avtp_pruned_layout(None, dl.ref(), p, p, p, p, p, p, None, p) == A.ERR_INVALID_ARG
+
+
+def test_select_compact_arguments_rejected_on_host():
+    lib = A.lib()
+    buf = torch.zeros(256, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    dl = _dl()
+    t = (A._Tensor * 1)()
+    assert lib.avtp_select_compact(None, None, p, p, p, 100, p, None, t, 0) == A.ERR_INVALID_ARG
+    assert lib.avtp_select_compact(None, dl.ref(), None, p, p, 100, p, None, t, 0) == A.ERR_INVALID_ARG
+    assert lib.avtp_select_compact(None, dl.ref(), p, p, p, 1, p, None, t, 0) == A.ERR_INVALID_ARG  # capacity
+    assert lib.avtp_select_compact(None, dl.ref(), p, p, p, 100, p, None, t, 9) == A.ERR_UNSUPPORTED
+    assert lib.avtp_select_compact(None, dl.ref(), p, p, p, 100, p, None, t, 1) == A.ERR_INVALID_ARG  # null src
