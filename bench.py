@@ -247,8 +247,8 @@ def main():
         calibrate_copy(args.calibrate_copy)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
-                                   "(the per-sequence path shards over sequences, see DESIGN.md)"}))
+        print(json.dumps({"error": "runs on one GPU only; --gpus must be 1 (the path is per "
+                                   "sequence and would shard over sequences across GPUs)"}))
         sys.exit(2)
     import torch
     from paper_2608_26806_amd import avtp as A

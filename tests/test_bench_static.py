@@ -1,6 +1,6 @@
 """bench.py on the CPU: it parses, and every name a function reads is defined
 (an argument, a local, a module-level name or a builtin).  bench.py only runs
-on a GPU machine, so this catches a missing import before it gets there."""
+where there is a GPU, so this catches a missing import on the CPU first."""
 import ast
 import builtins
 import os

@@ -47,7 +47,7 @@ def test_small_configs(cfg):
 
 
 def test_layout_shapes_of_all_configs():
-    """Layout-only draws for the large configurations (tensor draws are exercised on the GPU machine)."""
+    """Layout-only draws for the large configurations (tensor draws are exercised by the GPU tests)."""
     expect_T = {1: 16, 2: 64, 3: 96, 4: 128, 5: 512}
     for cfg, c in W.CONFIGS.items():
         imgs = W._image_sizes(cfg, c["B"], W._rng(cfg, W._S_LAYOUT))
