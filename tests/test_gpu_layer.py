@@ -109,3 +109,13 @@ def test_layer_select_hand_example():
     rs, sel = A.layer_select(torch.from_numpy(A_).cuda(), 2)
     assert rs.cpu().numpy().tolist() == [5, 7, 7, 11]
     assert sel.cpu().numpy().tolist() == [0, 1]
+
+
+def test_layer_select_max_layers_single_sample():
+    L, N = 1024, 1
+    A_ = _table(L, N, seed=99)
+    rs, sel = A.layer_select(torch.from_numpy(A_).cuda(), 10)
+    rs_o, _, sel_o = O.layer_select(A_.astype(np.float64), 10)
+    assert np.array_equal(rs.cpu().numpy().astype(np.int64), rs_o)
+    assert sel.cpu().numpy().tolist() == sel_o
+    assert sorted(rs.cpu().numpy().tolist()) == list(range(1, L + 1))   # one sample: a permutation

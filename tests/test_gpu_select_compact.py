@@ -105,3 +105,37 @@ def test_fused_equals_separate_calls(cfg):
     assert torch.equal(keep_a, keep_b) and torch.equal(cu_a, cu_b)
     for x, y in zip(outs_a, outs_b):
         assert np.array_equal(to_host_bits(x), to_host_bits(y))
+
+
+def test_fused_budgets_over_keep_total_flag_and_stay_in_bounds():
+    # budgets that sum past keep_total: keep_idx is written up to its capacity
+    # (and the overflow flagged) exactly as avtp_select does; rows are copied
+    # only below n_out, so outputs sized for n_out are never overrun
+    lay = build_layout([[40, 30], [25]], 2, 3, 50)
+    rng = np.random.default_rng(5)
+    s = rng.standard_normal(lay.N_tok).astype(np.float32)
+    budgets = np.array([30, 20, 20], np.int32)                  # keep_total is 35 and 13;
+    # sequence 0 writes entries [0, 57), sequence 1 [57, 82): past cap = n_out + 4 = 64
+    dl = A.DeviceLayout(lay)
+    n_out = dl.N_out
+    cap = n_out + 4                                              # some spare entries in keep_idx
+    say("[select_compact] over-full budgets")
+    hid = torch.randn(lay.N_tok, 48, device="cuda")
+    guard = torch.full((n_out + 8, 48), 7.0, device="cuda")     # rows past n_out must stay 7
+    out = guard[:n_out]
+    keep_f = torch.full((cap,), -1, dtype=torch.int32, device="cuda")
+    st_f = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+    keep_f, cu_f = A.select_compact(dl, torch.from_numpy(s).cuda(), torch.from_numpy(budgets).cuda(),
+                                    [(hid, out, 0)], keep_idx=keep_f, status=st_f)
+    keep_s = torch.full((cap,), -1, dtype=torch.int32, device="cuda")
+    st_s = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+    A.select(dl, torch.from_numpy(s).cuda(), torch.from_numpy(budgets).cuda(), keep_idx=keep_s,
+             status=st_s)
+    torch.cuda.synchronize()
+    st = st_f.cpu().numpy()
+    assert st.tolist() == st_s.cpu().numpy().tolist()
+    assert st.tolist() == [0, A.FLAG_OUT_CAPACITY]               # only the second sequence overflows
+    ks = keep_s.cpu().numpy()[:n_out]
+    assert keep_f.cpu().numpy()[:n_out].tolist() == ks.tolist()
+    assert torch.equal(out, hid[torch.from_numpy(ks.astype(np.int64)).cuda()])
+    assert torch.all(guard[n_out:] == 7.0)
