@@ -19,7 +19,6 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kBlockBytes = 32768;  // target bytes per block
-constexpr int kRowsInFlight = 4;    // rows a thread group copies at once (copy_rows)
 
 struct CArgs {
   CTensor t[AVTP_MAX_TENSORS];
@@ -29,71 +28,18 @@ struct CArgs {
   int N_tok;
 };
 
-// A thread group works on four rows at once: their keep_idx entries are
-// loaded together, then every row's vector units, then the stores, so that
-// several independent loads per lane are in flight (HBM latency is the limit
-// otherwise).  The rows are named variables, not arrays, so that they stay in
-// registers.
-template <typename V>
-struct RowJob {
-  const V *s;
-  V *d;
-  bool ok;
-};
-
-template <typename V>
-__device__ inline RowJob<V> row_job(const int32_t *__restrict__ keep_idx, long long r, long long r1,
-                                    int N_tok, const char *src, long long sstr, char *dst,
-                                    long long dstr) {
-  const int j = r < r1 ? keep_idx[r] : -1;
-  RowJob<V> w;
-  w.ok = (unsigned)j < (unsigned)N_tok;  // out-of-range index: row left untouched
-  w.s = reinterpret_cast<const V *>(src + (w.ok ? j : 0) * sstr);
-  w.d = reinterpret_cast<V *>(dst + (w.ok ? r : 0) * dstr);
-  return w;
-}
-
 template <typename V>
 __device__ inline void copy_rows(const CTensor &T, const int32_t *__restrict__ keep_idx,
                                  long long r0, long long r1, int N_tok, int plane) {
-  const int tid = threadIdx.x;
-  const int lpr = 1 << T.lpr_shift;
-  const int lane = tid & (lpr - 1);
+  const int lane = threadIdx.x & ((1 << T.lpr_shift) - 1);
   const long long rpp = kThreads >> T.lpr_shift;  // rows per pass of the block
-  const char *src = T.src + plane * T.src_plane_stride;
-  char *dst = T.dst + plane * T.dst_plane_stride;
-  const long long sstr = T.src_stride, dstr = T.dst_stride;
-  const int units = T.units;
-  for (long long rb = r0 + (tid >> T.lpr_shift); rb < r1; rb += kRowsInFlight * rpp) {
-    const RowJob<V> w0 = row_job<V>(keep_idx, rb, r1, N_tok, src, sstr, dst, dstr);
-    const RowJob<V> w1 = row_job<V>(keep_idx, rb + rpp, r1, N_tok, src, sstr, dst, dstr);
-    const RowJob<V> w2 = row_job<V>(keep_idx, rb + 2 * rpp, r1, N_tok, src, sstr, dst, dstr);
-    const RowJob<V> w3 = row_job<V>(keep_idx, rb + 3 * rpp, r1, N_tok, src, sstr, dst, dstr);
-    for (int u = lane; u < units; u += 2 * lpr) {
-      const bool two = u + lpr < units;
-      V a0{}, a1{}, a2{}, a3{}, b0{}, b1{}, b2{}, b3{};
-      auto ld = [&](const RowJob<V> &w, V &x, V &y) __attribute__((always_inline)) {
-        if (w.ok) {
-          x = w.s[u];
-          if (two) y = w.s[u + lpr];
-        }
-      };
-      auto st = [&](const RowJob<V> &w, const V &x, const V &y) __attribute__((always_inline)) {
-        if (w.ok) {
-          w.d[u] = x;
-          if (two) w.d[u + lpr] = y;
-        }
-      };
-      ld(w0, a0, b0);
-      ld(w1, a1, b1);
-      ld(w2, a2, b2);
-      ld(w3, a3, b3);
-      st(w0, a0, b0);
-      st(w1, a1, b1);
-      st(w2, a2, b2);
-      st(w3, a3, b3);
-    }
-  }
+  copy_rows_batched<V>(T, plane, r0 + (threadIdx.x >> T.lpr_shift), r1, rpp, lane,
+                       [&](long long r, long long &j, long long &dr) __attribute__((always_inline)) {
+                         const int k = keep_idx[r];
+                         j = k;
+                         dr = r;
+                         return (unsigned)k < (unsigned)N_tok;  // out-of-range index: row left untouched
+                       });
 }
 
 __global__ __launch_bounds__(kThreads) void compact_kernel(CArgs a) {

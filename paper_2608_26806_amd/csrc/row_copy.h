@@ -56,20 +56,72 @@ inline void describe_tensor(const avtp_tensor &x, int threads, CTensor &T) {
   T.rows_per_block = T.blocks_per_plane = T.block_begin = 0;
 }
 
-// Copy source row `j` of plane `plane` to destination row `r` with the
-// `lpr` lanes of one group (lane = this thread's index in its group).
+// Batched row copies: a lane group works on four rows at once (their source
+// and destination rows first, then every row's vector units, then the
+// stores), so that several independent loads per lane are in flight; HBM
+// latency is the limit otherwise.  The rows are named variables, not arrays,
+// so that they stay in registers.  entry(e, j, r) gives list entry e's source
+// row j and destination row r and returns false to skip it; the group handles
+// entries e0, e0 + step, ... below e1.
+constexpr int kRowsInFlight = 4;
+
 template <typename V>
-__device__ inline void copy_one_row(const CTensor &T, int plane, long long j, long long r, int lane) {
+struct RowJob {
+  const V *s;
+  V *d;
+  bool ok;
+};
+
+template <typename V, typename Entry>
+__device__ inline RowJob<V> row_job(Entry &entry, long long e, long long e1, const char *src,
+                                    long long sstr, char *dst, long long dstr) {
+  long long j = 0, r = 0;
+  RowJob<V> w;
+  w.ok = e < e1 && entry(e, j, r);
+  if (!w.ok) j = r = 0;
+  w.s = reinterpret_cast<const V *>(src + j * sstr);
+  w.d = reinterpret_cast<V *>(dst + r * dstr);
+  return w;
+}
+
+template <typename V, typename Entry>
+__device__ inline void copy_rows_batched(const CTensor &T, int plane, long long e0, long long e1,
+                                         long long step, int lane, Entry entry) {
   const int lpr = 1 << T.lpr_shift;
-  const V *s = reinterpret_cast<const V *>(T.src + plane * T.src_plane_stride + j * T.src_stride);
-  V *d = reinterpret_cast<V *>(T.dst + plane * T.dst_plane_stride + r * T.dst_stride);
-  int u = lane;
-  for (; u + lpr < T.units; u += 2 * lpr) {  // two independent loads in flight
-    const V a = s[u], b = s[u + lpr];
-    d[u] = a;
-    d[u + lpr] = b;
+  const char *src = T.src + plane * T.src_plane_stride;
+  char *dst = T.dst + plane * T.dst_plane_stride;
+  const long long sstr = T.src_stride, dstr = T.dst_stride;
+  const int units = T.units;
+  for (long long e = e0; e < e1; e += kRowsInFlight * step) {
+    const RowJob<V> w0 = row_job<V>(entry, e, e1, src, sstr, dst, dstr);
+    const RowJob<V> w1 = row_job<V>(entry, e + step, e1, src, sstr, dst, dstr);
+    const RowJob<V> w2 = row_job<V>(entry, e + 2 * step, e1, src, sstr, dst, dstr);
+    const RowJob<V> w3 = row_job<V>(entry, e + 3 * step, e1, src, sstr, dst, dstr);
+    for (int u = lane; u < units; u += 2 * lpr) {
+      const bool two = u + lpr < units;
+      V a0{}, a1{}, a2{}, a3{}, b0{}, b1{}, b2{}, b3{};
+      auto ld = [&](const RowJob<V> &w, V &x, V &y) __attribute__((always_inline)) {
+        if (w.ok) {
+          x = w.s[u];
+          if (two) y = w.s[u + lpr];
+        }
+      };
+      auto st = [&](const RowJob<V> &w, const V &x, const V &y) __attribute__((always_inline)) {
+        if (w.ok) {
+          w.d[u] = x;
+          if (two) w.d[u + lpr] = y;
+        }
+      };
+      ld(w0, a0, b0);
+      ld(w1, a1, b1);
+      ld(w2, a2, b2);
+      ld(w3, a3, b3);
+      st(w0, a0, b0);
+      st(w1, a1, b1);
+      st(w2, a2, b2);
+      st(w3, a3, b3);
+    }
   }
-  if (u < T.units) d[u] = s[u];
 }
 
 }  // namespace avtp

@@ -294,15 +294,19 @@ struct SCArgs {
 };
 
 // The listed rows of one tensor, a power-of-two group of lanes per row (as in
-// the compaction kernel).
+// the compaction kernel), four rows per group at once.
 template <typename V>
 __device__ inline void copy_listed(const CTensor &T, const int *lo, const int *lj, int n) {
   const int lpr_shift = T.lpr_shift;
   const int lane = threadIdx.x & ((1 << lpr_shift) - 1);
   const int per_pass = kThreads >> lpr_shift;
   for (int p = 0; p < T.planes; ++p)
-    for (int e = (int)(threadIdx.x >> lpr_shift); e < n; e += per_pass)
-      copy_one_row<V>(T, p, lj[e], lo[e], lane);
+    copy_rows_batched<V>(T, p, (long long)(threadIdx.x >> lpr_shift), n, per_pass, lane,
+                         [&](long long e, long long &j, long long &r) __attribute__((always_inline)) {
+                           j = lj[e];
+                           r = lo[e];
+                           return true;
+                         });
 }
 
 __global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a) {
