@@ -935,6 +935,27 @@ __global__ __launch_bounds__(256) void finalize_kernel(
   __syncthreads();
   const int b = sh_b;
   const int s0 = img_start[i], n = img_len[i];
+  // Tokens j = tid + 256 q (q < 4) of the first 1024 are summed over the
+  // planes before the text-row count, so that all their loads are in flight
+  // together; every token's plane sum runs in plane order either way.
+  float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
+  if (colsum) {
+    const float *c0 = colsum + s0 + tid;
+    // a token past the image re-reads token tid (in bounds); its sum is not used
+    const int o1 = tid + 256 < n ? 256 : 0, o2 = tid + 512 < n ? 512 : 0,
+              o3 = tid + 768 < n ? 768 : 0;
+    if (tid < n) {
+#pragma unroll 4
+      for (int g = 0; g < planes; ++g) {
+        const float *cg = c0 + (size_t)g * N_tok;
+        const float x0 = cg[0], x1 = cg[o1], x2 = cg[o2], x3 = cg[o3];
+        v0 += x0;
+        v1 += x1;
+        v2 += x2;
+        v3 += x3;
+      }
+    }
+  }
   int nT = 0;
   if (colsum) {  // text rows after the image (their positions exceed s0)
     int c = 0;
@@ -950,8 +971,14 @@ __global__ __launch_bounds__(256) void finalize_kernel(
   for (int j = tid; j < n; j += 256) {
     float s;
     if (colsum) {
-      float v = 0.f;
-      for (int g = 0; g < planes; ++g) v += colsum[(size_t)g * N_tok + s0 + j];
+      float v;
+      if (j < 1024) {
+        const int q = (j - tid) >> 8;
+        v = q == 0 ? v0 : (q == 1 ? v1 : (q == 2 ? v2 : v3));
+      } else {
+        v = 0.f;
+        for (int g = 0; g < planes; ++g) v += colsum[(size_t)g * N_tok + s0 + j];
+      }
       s = nT > 0 ? v / (float)((long long)Hq * nT) : 0.f;
       scores[s0 + j] = s;
     } else {
