@@ -582,12 +582,33 @@ __global__ void lse_combine_kernel(const float *__restrict__ part_m, const float
                                    float *__restrict__ lse2) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= rows) return;
+  // Chunks in groups of 8 whose loads are issued together (a chunk index past
+  // nkc re-reads the last chunk and is then ignored); max and sum run over
+  // the chunks in ascending order.
+  constexpr int kGroup = 8;
+  auto at = [&](int c) __attribute__((always_inline)) {
+    return (size_t)min(c, nkc - 1) * rows + idx;
+  };
   float M = -INFINITY;
-  for (int c = 0; c < nkc; ++c) M = fmaxf(M, part_m[(size_t)c * rows + idx]);
+  for (int c0 = 0; c0 < nkc; c0 += kGroup) {
+    float m[kGroup];
+#pragma unroll
+    for (int u = 0; u < kGroup; ++u) m[u] = part_m[at(c0 + u)];
+#pragma unroll
+    for (int u = 0; u < kGroup; ++u)
+      if (c0 + u < nkc) M = fmaxf(M, m[u]);
+  }
   float S = 0.f;
-  for (int c = 0; c < nkc; ++c) {
-    const float m = part_m[(size_t)c * rows + idx];
-    if (m != -INFINITY) S += part_l[(size_t)c * rows + idx] * __builtin_amdgcn_exp2f(m - M);
+  for (int c0 = 0; c0 < nkc; c0 += kGroup) {
+    float m[kGroup], l[kGroup];
+#pragma unroll
+    for (int u = 0; u < kGroup; ++u) {
+      m[u] = part_m[at(c0 + u)];
+      l[u] = part_l[at(c0 + u)];
+    }
+#pragma unroll
+    for (int u = 0; u < kGroup; ++u)
+      if (c0 + u < nkc && m[u] != -INFINITY) S += l[u] * __builtin_amdgcn_exp2f(m[u] - M);
   }
   const float v = (M + __builtin_amdgcn_logf(S)) * kLn2;
   lse[idx] = v;

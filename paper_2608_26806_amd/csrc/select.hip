@@ -158,6 +158,13 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   const int k = eff_budget(budget, img_len, i);
   long long part = 0;  // budgets of the images before i
   for (int j = tid; j < i; j += kThreads) part += eff_budget(budget, img_len, j);
+  // the image's order keys into LDS now: their loads overlap the prefix and
+  // text-row reductions below (whose barriers also order them before the
+  // radix passes)
+  const bool in_lds = n <= kLdsKeys;
+  if (in_lds)
+#pragma unroll 4
+    for (int j = tid; j < n; j += kThreads) keys[j] = order_key(scores[st + j]);
   const long long pre = block_sum_ll(part, red);  // (also publishes sh_b)
   const int b = sh_b;
   const int a_lo = cu_text[b], a_hi = cu_text[b + 1];
@@ -202,9 +209,6 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   }
 
   // ---- radix select of the k-th largest key
-  const bool in_lds = n <= kLdsKeys;
-  if (in_lds)
-    for (int j = tid; j < n; j += kThreads) keys[j] = order_key(s[j]);
   uint32_t prefix = 0, mask = 0;
   int krem = k;
   for (int pass = 0; pass < 4; ++pass) {
