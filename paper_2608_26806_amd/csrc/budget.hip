@@ -120,6 +120,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
                                                           int floor_abs, int32_t *__restrict__ budget,
                                                           int32_t *__restrict__ status) {
   __shared__ uint64_t W[kMaxImg], rem[kMaxImg];
+  __shared__ uint64_t fpart[kThreads];  // partial f of a breakpoint, one per thread
   __shared__ int32_t lo[kMaxImg], hi[kMaxImg];
   __shared__ float sv[kMaxImg];
   __shared__ long long red_i[4];
@@ -175,16 +176,16 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
   __syncthreads();
 
   // Breakpoints k < m: lo_k / W_k, k >= m: hi_(k-m) / W_(k-m) (zero-length
-  // images have none).  Each thread evaluates f at its breakpoints and keeps
-  // the smallest with f >= K (next) and the largest with f < K (prev).
+  // images have none).  f is evaluated at every breakpoint; each thread keeps
+  // the smallest breakpoint with f >= K (next) and the largest with f < K
+  // (prev).  With few breakpoints, np threads share one breakpoint's sum
+  // over the images (np parts, combined in LDS; integer sums, so exact).
   bool hn = false, hp = false;
   uint64_t bn = 0, bd = 1, pn = 0, pd = 1;
-  for (int k = tid; k < 2 * m; k += kThreads) {
-    const int i = k < m ? k : k - m;
-    if (W[i] == 0) continue;
-    const uint64_t num = (uint64_t)(k < m ? lo[i] : hi[i]), den = W[i];
-    uint64_t f = 0;  // f(num/den) * den
-    for (int j = 0; j < m; ++j) {
+  auto partial_f = [&](uint64_t num, uint64_t den, int j0, int j1) __attribute__((always_inline)) {
+    uint64_t f = 0;  // f(num/den) * den over images j0 .. j1-1
+#pragma unroll 4
+    for (int j = j0; j < j1; ++j) {
       const uint64_t wj = W[j];
       if (wj == 0) continue;
       uint64_t v = num * wj;
@@ -192,16 +193,50 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
       v = v < lj ? lj : (v > hj ? hj : v);
       f += v;
     }
-    if (f >= (uint64_t)K * den) {
-      if (!hn || frac_lt(num, den, bn, bd)) {
-        bn = num;
-        bd = den;
-        hn = true;
+    return f;
+  };
+  auto keep_ext = [&](uint64_t f, uint64_t num, uint64_t den) __attribute__((always_inline)) {
+    // value selects (not stores through a chosen reference), so that the six
+    // values stay in registers
+    const bool ge = f >= (uint64_t)K * den;
+    const bool tn = ge && (!hn || frac_lt(num, den, bn, bd));
+    const bool tp = !ge && (!hp || frac_lt(pn, pd, num, den));
+    bn = tn ? num : bn;
+    bd = tn ? den : bd;
+    hn = hn || tn;
+    pn = tp ? num : pn;
+    pd = tp ? den : pd;
+    hp = hp || tp;
+  };
+  const int nbp = 2 * m;
+  const int np = nbp <= kThreads / 4 ? 4 : (nbp <= kThreads / 2 ? 2 : 1);  // parts; block-uniform
+  if (np > 1) {
+    const int KB = kThreads / np;  // >= nbp
+    const int k = tid % KB, part = tid / KB;
+    const int per = (m + np - 1) / np, j0 = min(m, part * per), j1 = min(m, j0 + per);
+    bool ok = false;
+    uint64_t num = 0, den = 1, f = 0;
+    if (k < nbp) {
+      const int i = k < m ? k : k - m;
+      if (W[i] != 0) {
+        ok = true;
+        num = (uint64_t)(k < m ? lo[i] : hi[i]);
+        den = W[i];
+        f = partial_f(num, den, j0, j1);
       }
-    } else if (!hp || frac_lt(pn, pd, num, den)) {
-      pn = num;
-      pd = den;
-      hp = true;
+    }
+    fpart[tid] = f;
+    __syncthreads();
+    if (part == 0 && ok) {
+      for (int q = 1; q < np; ++q) f += fpart[q * KB + k];
+      keep_ext(f, num, den);
+    }
+  } else {
+    for (int k = tid; k < nbp; k += kThreads) {
+      const int i = k < m ? k : k - m;
+      if (W[i] == 0) continue;
+      const uint64_t num = (uint64_t)(k < m ? lo[i] : hi[i]), den = W[i];
+      keep_ext(partial_f(num, den, 0, m), num, den);
     }
   }
   block_frac_ext<true>(bn, bd, hn, ext_n, ext_d, ext_o);

@@ -132,6 +132,15 @@ def _budget_cases():
         if t % 13 == 5:
             S[int(rng.integers(0, m))] = 0.0
         cases.append((n, S, alpha, floor_abs, mode))
+    # more images per sequence than 32: the kernel splits each breakpoint's
+    # sum over 4 threads up to 32 images, over 2 up to 64, and not above
+    for t, m in enumerate([33, 48, 64, 65, 100, 128, 129, 200, 256]):
+        n = [int(x) for x in rng.integers(1, 400, size=m)]
+        alpha = [1.0, 2.0, 0.0][t % 3]
+        floor_abs = [0, 16][t % 2]
+        mode = O.BUDGET_RAW if t % 4 == 3 else O.BUDGET_PROPORTIONAL
+        S = (rng.lognormal(0.0, 2.0, size=m) * np.array(n) / 100).astype(np.float32)
+        cases.append((n, S, alpha, floor_abs, mode))
     return cases
 
 
@@ -156,6 +165,27 @@ def test_budget_bit_exact_on_same_image_sums():
         o = O.budget(lay, S, alpha, 50, 950, fa, mode)
         assert np.array_equal(g, o), (n, S, alpha, fa, mode, K, g, o)
         assert not status.any()
+
+
+def test_budget_mixed_image_counts_one_launch():
+    # sequences of 10, 50 and 150 images in one launch: their blocks take the
+    # three ways of splitting the breakpoint sums
+    rng = np.random.default_rng(19)
+    seqs = [[int(x) for x in rng.integers(1, 300, size=m)] for m in (10, 50, 150)]
+    lay = build_layout(seqs, 2, 3, 0)
+    keeps = []
+    for n in seqs:
+        lo = sum(O.budget_bounds(x, 50, 950, 8)[0] for x in n)
+        hi = sum(O.budget_bounds(x, 50, 950, 8)[1] for x in n)
+        keeps.append(int(rng.integers(lo, hi + 1)))
+    lay.keep_total[:] = keeps
+    dl = A.DeviceLayout(lay)
+    S = (rng.lognormal(0.0, 1.5, size=lay.n_img) * lay.img_len / 100).astype(np.float32)
+    say("[budget] mixed image counts 10/50/150")
+    status = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+    g = A.budget(dl, torch.from_numpy(S).cuda(), 1.0, 50, 950, 8, status=status).cpu().numpy()
+    assert np.array_equal(g, O.budget(lay, S, 1.0, 50, 950, 8))
+    assert not status.any()
 
 
 @pytest.mark.parametrize("K_at", ["lo", "hi"])
