@@ -194,7 +194,8 @@ int avtp_select(avtp_stream_t stream, const avtp_layout *layout, const float *sc
  * AVTP_MAX_TENSORS tensors in one launch (hidden states, position ids with
  * their original values, K and V of the layer).  n_out = number of entries
  * of keep_idx to apply (normally T_tot + sum(keep_total)); every keep_idx
- * entry must lie in [0, N_tok).  tensors: HOST array of n_tensors
+ * entry should lie in [0, N_tok): an entry outside it reads nothing and
+ * leaves its output row as it was.  tensors: HOST array of n_tensors
  * descriptors.  Copies are bit-exact.
  * ---------------------------------------------------------------------- */
 int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t *keep_idx,

@@ -277,6 +277,37 @@ def test_compact_odd_row_sizes():
         assert torch.equal(out.cpu(), x.cpu()[torch.from_numpy(keep).long()])
 
 
+def test_compact_out_of_range_index_leaves_row():
+    # entries -1 and >= N_tok, some in the middle of a thread group's four
+    # rows: those output rows keep what they held, all others are copied
+    lay = build_layout([[300, 40], [129]], 3, 5, 50)
+    dl = A.DeviceLayout(lay)
+    N, n_out = lay.N_tok, dl.N_out
+    rng = np.random.default_rng(11)
+    keep = np.sort(rng.choice(N, n_out, replace=False)).astype(np.int32)
+    bad = rng.choice(n_out, 9, replace=False)
+    keep[bad[:5]] = -1
+    keep[bad[5:]] = N + np.arange(4, dtype=np.int32)
+    good = np.ones(n_out, bool)
+    good[bad] = False
+    keep_d = torch.from_numpy(keep).cuda()
+    idx = torch.from_numpy(keep[good].astype(np.int64)).cuda()
+    gd = torch.from_numpy(good).cuda()
+    say("[compact] out-of-range indices")
+    for shape, dt, tdim in [((N, 64), torch.bfloat16, 0), ((3, N), torch.int64, 1),
+                            ((N, 4096), torch.bfloat16, 0), ((N, 3), torch.uint8, 0)]:
+        x = torch.randint(0, 100, shape, dtype=torch.int32).to(dt).cuda()
+        oshape = list(shape)
+        oshape[tdim] = n_out
+        out = torch.full(oshape, 7, dtype=dt, device="cuda")
+        A.compact(dl, keep_d, [(x, out, tdim)])
+        torch.cuda.synchronize()
+        if tdim == 0:
+            assert torch.equal(out[gd], x[idx]) and torch.all(out[~gd] == 7)
+        else:
+            assert torch.equal(out[:, gd], x[:, idx]) and torch.all(out[:, ~gd] == 7)
+
+
 # ------------------------------------------------------------------ end to end
 @pytest.mark.parametrize("cfg", [1, 2, 3])
 def test_end_to_end(cfg):
