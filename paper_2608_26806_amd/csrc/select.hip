@@ -128,12 +128,12 @@ struct SelArgs {
 // put(output index, token index, sequence) in no particular order.
 template <typename Put>
 __device__ __attribute__((always_inline)) inline void select_image(const SelArgs &A, int i, Put put) {
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hist[2][256];  // double-buffered across the radix passes
   __shared__ uint32_t keys[kLdsKeys];
   __shared__ int wsum[4];
   __shared__ long long red[4];
-  __shared__ uint32_t sh_digit;
-  __shared__ int sh_krem, sh_b;
+  __shared__ uint32_t sh_digit[4];  // one slot per radix pass
+  __shared__ int sh_krem[4], sh_b;
   const int tid = threadIdx.x;
   const float *__restrict__ scores = A.scores;
   const int32_t *__restrict__ budget = A.budget;
@@ -165,6 +165,7 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   if (in_lds)
 #pragma unroll 4
     for (int j = tid; j < n; j += kThreads) keys[j] = order_key(scores[st + j]);
+  hist[0][tid] = 0;  // the first radix pass's histogram (kThreads == 256 bins)
   const long long pre = block_sum_ll(part, red);  // (also publishes sh_b)
   const int b = sh_b;
   const int a_lo = cu_text[b], a_hi = cu_text[b + 1];
@@ -211,21 +212,23 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   // ---- radix select of the k-th largest key
   uint32_t prefix = 0, mask = 0;
   int krem = k;
+  // Two barriers per pass: pass p counts into hist[p & 1] (cleared during
+  // pass p - 1, or above for p = 0) while the other buffer, last read by
+  // pass p - 1's digit pick, is cleared for pass p + 1.
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    hist[tid] = 0;
-    __syncthreads();
+    uint32_t *h = hist[pass & 1];
     for (int j = tid; j < n; j += kThreads) {
       const uint32_t key = in_lds ? keys[j] : order_key(s[j]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
     }
-    __syncthreads();
-    pick_digit(hist, krem, &sh_digit, &sh_krem);
-    __syncthreads();
-    prefix |= sh_digit << shift;
+    __syncthreads();  // the histogram is complete
+    pick_digit(h, krem, &sh_digit[pass], &sh_krem[pass]);
+    hist[(pass + 1) & 1][tid] = 0;
+    __syncthreads();  // the digit is published and the next buffer is clear
+    prefix |= sh_digit[pass] << shift;
     mask |= 255u << shift;
-    krem = sh_krem;
-    __syncthreads();
+    krem = sh_krem[pass];
   }
   const uint32_t theta = prefix;  // exactly krem keys equal to theta are kept
 
