@@ -161,8 +161,10 @@ int avtp_row_lse(avtp_stream_t stream, const avtp_layout *layout, int dtype, con
  *   RAW:          w_i = n_i/M + alpha (S_i - n_i S/M) / K
  * (each the ratio r_i = r_base + alpha (Ibar_i - Ibar_avg) of the paper with
  * r_base = K/M; PROPORTIONAL measures importance in units of its mean).
- * w_i < 0 -> 0; W_i = max(1, rint(w_i * 2^28)), float64, no FMA contraction;
- * if S is not positive and finite, w_i = n_i/M.  Bounds
+ * w_i < 0 -> 0; only the ratios of the shares matter, so with w_max the
+ * largest share of the sequence W_i = max(1, rint((w_i / w_max) * 2^28))
+ * (float64, one operation at a time, no FMA contraction); if S is not
+ * positive and finite, w_i = n_i/M.  Bounds
  *   lo_i = min(n_i, max(ceil(lo_permille n_i / 1000), floor_abs)),
  *   hi_i = max(lo_i, floor(hi_permille n_i / 1000))
  * (paper: 5 % and 95 %, i.e. 50 and 950).  Exact integer water-filling finds
@@ -176,22 +178,34 @@ int avtp_budget(avtp_stream_t stream, const avtp_layout *layout, const float *im
                 int32_t *status);
 
 /* ------------------------------------------------------------------------
- * avtp_select -- keep, inside every image, the budget[i] highest-scoring
- * tokens (score descending; an exact tie keeps the lowest token index; -0.0
- * equals +0.0; NaN ranks last), plus every text token.  Writes the kept
- * global token indices of each sequence in ascending order to
- * keep_idx[cu_out[b] .. cu_out[b+1]), and cu_out [B+1].
+ * avtp_select -- the pruned subsequence (Method, "Visual Token Pruning": the
+ * pruning map keeps a subset of the visual tokens and every text token),
+ * with the per-image keep counts of Sec. 3.3.3 (an image keeps budget[i]
+ * tokens, so more important images keep more).  Inside every image the
+ * budget[i] highest-scoring tokens are kept (score descending; an exact tie
+ * keeps the lowest token index; -0.0 equals +0.0; NaN ranks last), plus
+ * every text token.  Writes the kept global token indices of each sequence
+ * in ascending order to keep_idx[cu_out[b] .. cu_out[b+1]), and cu_out [B+1].
+ *   scores [N_tok] fp32 (device; text positions are not read), budget
+ *   [n_img] int32 (device), keep_idx [keep_capacity] int32 and cu_out [B+1]
+ *   int32 (device outputs).
  * keep_capacity: entries available in keep_idx; must be at least
  * T_tot + sum(keep_total) (checked on the host); writes past it are dropped
  * and flag AVTP_FLAG_OUT_CAPACITY (budgets not summing to keep_total).
+ * No workspace: the selection of an image runs inside one block, from its
+ * keys cached in LDS (or re-read from scores for images above 4096 tokens),
+ * and each block knows its output offset from the budgets; so there is no
+ * avtp_select_workspace_size.
  * ---------------------------------------------------------------------- */
 int avtp_select(avtp_stream_t stream, const avtp_layout *layout, const float *scores,
                 const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out,
                 int32_t *status);
 
 /* ------------------------------------------------------------------------
- * avtp_compact -- stable gather out[r] = in[keep_idx[r]] for up to
- * AVTP_MAX_TENSORS tensors in one launch (hidden states, position ids with
+ * avtp_compact -- the pruned sequence that the following layers run on
+ * (Method, "Visual Token Pruning": E_pruned replaces E_v; Sec. 3.3.3: the
+ * kept tokens of each image): stable gather out[r] = in[keep_idx[r]] for up
+ * to AVTP_MAX_TENSORS tensors in one launch (hidden states, position ids with
  * their original values, K and V of the layer).  n_out = number of entries
  * of keep_idx to apply (normally T_tot + sum(keep_total)); every keep_idx
  * entry should lie in [0, N_tok): an entry outside it reads nothing and

@@ -209,8 +209,7 @@ def variation_scores(layout, h_cur, h_prior, dtype: str):
 # ---------------------------------------------------------------------------
 # O2: per-image budgets (Sec. 3.3.3 + Appendix clamp)
 # ---------------------------------------------------------------------------
-WEIGHT_BITS = 28          # the quantisation grid of the per-image weights
-WEIGHT_CAP = 64.0         # largest per-image weight
+WEIGHT_BITS = 28          # the largest weight becomes 2^28; the others keep their ratio to it
 BUDGET_PROPORTIONAL = 0   # r_i in units where the mean importance equals r_base
 BUDGET_RAW = 1            # r_i = r_base + alpha (I_i - I_avg) in raw score units
 
@@ -232,11 +231,14 @@ def budget_weights(n_list, S_list, K: int, alpha: float, mode: int = BUDGET_PROP
                       -> w_i = (1 - alpha) n_i / M + alpha S_i / S
         raw:          r_i = r_base + alpha (Ibar_i - Ibar_avg)
                       -> w_i = n_i / M + alpha (S_i - n_i S / M) / K
-    Negative w are clamped to 0 and w above 64 to 64 (keeps the integer
-    stage within 63-bit products); W_i = max(1, rint(w_i 2^28)) so that every
-    image stays in the water-filling.  If S is not positive and finite, every
-    image gets its token share n_i / M.  Each operation is one IEEE float64
-    operation, evaluated left to right, no fused multiply-add.
+    Negative w are clamped to 0.  Only the ratios of the weights matter to the
+    water-filling (q_i = clamp(lam W_i, ...)), so they are measured against the
+    largest one, w_max: W_i = max(1, rint((w_i / w_max) 2^28)).  This keeps
+    every ratio of the rule (to 2^-28 of the largest weight) for weights of any
+    size and bounds the integer stage's products; W_i >= 1 keeps every image in
+    the water-filling.  If S is not positive and finite, every image gets its
+    token share n_i / M.  Each operation is one IEEE float64 operation,
+    evaluated left to right, no fused multiply-add.
     """
     alpha = float(np.float32(alpha))
     M = 0
@@ -246,11 +248,11 @@ def budget_weights(n_list, S_list, K: int, alpha: float, mode: int = BUDGET_PROP
     for s in S_list:
         S = S + float(np.float32(s))
     good = math.isfinite(S) and S > 0.0
-    W = []
+    ws = []
     for n, s in zip(n_list, S_list):
         s = float(np.float32(s))
         if int(n) == 0:
-            W.append(0)
+            ws.append(None)
             continue
         u = float(n) / float(M)
         if not good or not math.isfinite(s):
@@ -261,9 +263,16 @@ def budget_weights(n_list, S_list, K: int, alpha: float, mode: int = BUDGET_PROP
             w = u + alpha * ((s - u * S) / float(K)) if K > 0 else u
         if not (w > 0.0):
             w = 0.0
-        if w > WEIGHT_CAP:
-            w = WEIGHT_CAP
-        W.append(max(1, int(round(w * float(1 << WEIGHT_BITS)))))
+        ws.append(w)
+    w_max = max([w for w in ws if w is not None], default=0.0)
+    W = []
+    for w in ws:
+        if w is None:
+            W.append(0)
+        elif w_max > 0.0:
+            W.append(max(1, int(round((w / w_max) * float(1 << WEIGHT_BITS)))))
+        else:
+            W.append(1)
     return W
 
 

@@ -3,10 +3,11 @@
 // image.
 //
 // The only floating-point step is the integer weight of every image,
-//   W_i = max(1, rint(min(w_i, 64) * 2^28)),
-// evaluated in IEEE float64 with no contraction, in a fixed operation order
-// (documented in include/avtp.h).  Everything after it is exact integer
-// arithmetic:
+//   W_i = max(1, rint((w_i / w_max) * 2^28))
+// (w_max the largest weight of the sequence: only the ratios of the weights
+// enter the water-filling), evaluated in IEEE float64 with no contraction,
+// in a fixed operation order (documented in include/avtp.h).  Everything
+// after it is exact integer arithmetic:
 //   * the real quota q_i = clamp(lam W_i, lo_i, hi_i) with sum q_i = K lies on
 //     the segment between two consecutive breakpoints lo_i/W_i, hi_i/W_i of
 //     f(lam) = sum_i clamp(lam W_i, lo_i, hi_i); every thread evaluates f at
@@ -16,8 +17,8 @@
 //     weights), so q_i = P W_i / Q for free images;
 //   * largest remainder: floor(q_i), then +1 for the K - sum floor images with
 //     the largest remainders (P W_i mod Q), lowest image index first.
-// Limits (checked on the host): n_i <= 2^20, <= 256 images per sequence,
-// alpha <= 32, so every product fits in 63 bits.
+// Limits (checked on the host): n_i <= 2^20 and <= 256 images per sequence;
+// with W_i <= 2^28 every product is below 2^48 and every sum below 2^56.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -29,9 +30,8 @@ namespace {
 
 constexpr int kMaxImg = AVTP_MAX_IMAGES_PER_SEQ;
 constexpr int kWeightBits = 28;
-constexpr double kWeightCap = 64.0;
 
-// a/b < c/d for positive denominators (all values < 2^31 * 2^35 in range)
+// a/b < c/d for positive denominators (numerators <= 2^20, denominators <= 2^28)
 __device__ inline bool frac_lt(uint64_t a, uint64_t b, uint64_t c, uint64_t d) {
   return a * d < c * b;
 }
@@ -57,7 +57,6 @@ __device__ double image_weight(int n, long long M, float s32, double S, bool goo
     w = u;
   }
   if (!(w > 0.0)) w = 0.0;
-  if (w > kWeightCap) w = kWeightCap;
   return w;
 }
 
@@ -126,7 +125,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
   __shared__ long long red_i[4];
   __shared__ uint64_t red_u[4], ext_n[4], ext_d[4];
   __shared__ int ext_o[4];
-  __shared__ double sh_S;
+  __shared__ double sh_S, red_d[4];
 
   const int b = blockIdx.x, tid = threadIdx.x;
   const int i0 = cu_img[b], m = cu_img[b + 1] - i0;
@@ -159,11 +158,23 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
   __syncthreads();
   const double S = sh_S;
   const bool good = isfinite(S) && S > 0.0;
+  double w = 0.0;
+  if (mine) w = image_weight((int)n, M, s32, S, good, mode, (double)alpha, (int)K);
+  // the largest weight (weights are >= 0; images without tokens have none)
+  double wmax = w;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) wmax = fmax(wmax, __shfl_xor(wmax, off));
+  if ((tid & 63) == 0) red_d[tid >> 6] = wmax;
+  __syncthreads();
+  wmax = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
   uint64_t Wi = 0;
   if (mine) {
-    const double w = image_weight((int)n, M, s32, S, good, mode, (double)alpha, (int)K);
     if (n > 0) {
-      Wi = (uint64_t)rint(w * (double)(1ll << kWeightBits));
+      if (wmax > 0.0) {
+#pragma clang fp contract(off)
+        const double r = w / wmax;
+        Wi = (uint64_t)rint(r * (double)(1ll << kWeightBits));
+      }
       if (Wi < 1) Wi = 1;
     }
     W[tid] = Wi;

@@ -154,3 +154,47 @@ def test_bf16_inputs_widen_exactly():
     w = O.widen(x, "bf16")
     ref = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).double().numpy()
     np.testing.assert_array_equal(w, ref)
+
+
+@pytest.mark.parametrize("case", ["config1", "interleaved_bf16_gqa"])
+def test_score_one_matches_full_scores(case):
+    """``attn_score_one`` (the per-token form that checks sampled tokens at full
+    size) against ``attn_scores`` for every visual token, rel 1e-12.
+
+    The interleaved case has text before every image, so the row set of a token
+    (the text rows after it) differs from image to image, and 8 query heads on
+    2 key heads, so a wrong head-to-group map (h % Hkv for h // G) changes every
+    score.  Text and visual positions never coincide, so "after" needs no
+    tie rule."""
+    if case == "config1":
+        wl = make_workload(1, payload=False)
+        lay, q, k, Hq, Hkv, scale, dt = (wl.layout, wl.q_text, wl.k, wl.Hq, wl.Hkv,
+                                         wl.softmax_scale, "fp32")
+    else:
+        rng = np.random.default_rng(21)
+        lay = build_layout([[9, 1, 14], [5, 7]], 3, 4, 50)
+        Hq, Hkv, d = 8, 2, 64
+        from paper_2608_26806_amd.workloads import f32_to_bf16_bits
+        q = f32_to_bf16_bits(rng.standard_normal((lay.T_tot, Hq, d)).astype(np.float32))
+        k = f32_to_bf16_bits(rng.standard_normal((lay.N_tok, Hkv, d)).astype(np.float32))
+        scale, dt = d ** -0.5, "bf16"
+    s, _, lse, _ = O.attn_scores(lay, q, k, Hq, Hkv, scale, dt)
+    vis = np.flatnonzero(lay.visual_mask())
+    one = np.array([O.attn_score_one(lay, q, k, Hq, Hkv, scale, dt, lse, int(j)) for j in vis])
+    np.testing.assert_allclose(one, s[vis], rtol=1e-12, atol=0.0)
+    # the per-token form agrees with the loops-only brute force too (one
+    # sequence at a time: the brute force takes a single sequence)
+    if case == "interleaved_bf16_gqa":
+        qf, kf = O.widen(q, dt), O.widen(k, dt)
+        toks = _tokens(lay)
+        ref = {}
+        for b in range(lay.B):
+            s0, s1 = int(lay.cu_seqlens[b]), int(lay.cu_seqlens[b + 1])
+            t0 = int(lay.cu_text[b])
+            seq = [(kind, x - t0 if kind == "text" else x) for kind, x in toks[s0:s1]]
+            qs = [[list(map(float, qf[t, h])) for h in range(Hq)]
+                  for t in range(t0, int(lay.cu_text[b + 1]))]
+            ks = [[list(map(float, kf[j, g])) for g in range(Hkv)] for j in range(s0, s1)]
+            bs, _ = brute.attn_scores_loops(seq, qs, ks, Hq, Hkv, scale)
+            ref.update({s0 + p: v for p, v in enumerate(bs) if v is not None})
+        np.testing.assert_allclose(one, [ref[int(j)] for j in vis], rtol=1e-12, atol=0.0)

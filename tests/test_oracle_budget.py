@@ -185,9 +185,40 @@ def test_infeasible_and_degenerate():
     assert list(O.budget(lay, [5.0, 1.0], 1.0)) == [38, 38]
 
 
-def test_weights_quantisation_is_round_half_even_on_2_pow_28():
+def test_weights_quantisation_is_round_half_even_relative_to_the_largest():
+    # w = (0.25, 0.75): the largest becomes 2^28, the other 2^28 / 3 = 89478485.33 -> 89478485
     W = O.budget_weights([1, 1], [1.0, 3.0], 1, 1.0)
-    assert W == [1 << 26, 3 << 26]
+    assert W == [89478485, 1 << 28]
+    # w = (0.375, 0.625) = (3/8, 5/8): 3/5 * 2^28 = 161061273.6 -> 161061274
+    W = O.budget_weights([1, 1], [3.0, 5.0], 1, 1.0)
+    assert W == [161061274, 1 << 28]
+    # a tiny share keeps its ratio: S = (1, 2^24) -> 2^28 / 2^24 = 16
+    W = O.budget_weights([1, 1], [1.0, float(2 ** 24)], 1, 1.0)
+    assert W == [16, 1 << 28]
     # zero-importance images keep weight 1 (they only fill what the others cannot)
     W = O.budget_weights([5, 5], [0.0, 2.0], 1, 1.0)
     assert W == [1, 1 << 28]
+
+
+def test_raw_rule_keeps_ratios_of_large_weights():
+    """A hand-derived BUDGET_RAW case with shares far above 1, where only the
+    ratio of the weights decides the split (Sec. 3.3.3 ratio rule with
+    r_base = K / M, clamp of the appendix).
+
+    Four images of 64 tokens, M = 256, K = 98, alpha = 1, S = (24451, 34251, 0, 0)
+    (S = 58702, Ibar_avg = S / M = 229.3046875).  The literal rule gives
+        r_1 = 98/256 + (24451/64 - 229.3046875) = 153.125,  q_1 = 64 r_1 = 9800
+        r_2 = 98/256 + (34251/64 - 229.3046875) = 306.25,   q_2 = 19600
+        r_3 = r_4 = 98/256 - 229.3046875 = -228.921875,     q_3 = q_4 = -14651
+    (shares w = q / K = 100, 200, -149.5, -149.5; sum q = K).  Images 3 and 4
+    fall to their floor ceil(5 % of 64) = 4; the other 90 units are split in
+    the ratio 100 : 200 of the first two, i.e. (30, 60), with 60 = floor(95 %
+    of 64) just reached.  A cap on the shares (e.g. at 64) would make the two
+    equal and give (45, 45)."""
+    lay = _one_seq([64, 64, 64, 64], 98)
+    S = [24451.0, 34251.0, 0.0, 0.0]
+    W = O.budget_weights([64] * 4, S, 98, 1.0, mode=O.BUDGET_RAW)
+    assert W == [1 << 27, 1 << 28, 1, 1]
+    k, q = O.budget(lay, S, 1.0, mode=O.BUDGET_RAW, return_quota=True)
+    assert list(k) == [30, 60, 4, 4]
+    assert [float(x) for x in q] == [30.0, 60.0, 4.0, 4.0]

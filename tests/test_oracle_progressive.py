@@ -48,8 +48,7 @@ def test_two_layer_chain_invariants():
         s0, n = int(nxt.img_start[i]), int(nxt.img_len[i])
         src = keep[s0:s0 + n]
         assert all(lay.img_start[i] <= j < lay.img_start[i] + lay.img_len[i] for j in src)
-    assert nxt.keep_total.tolist() == [(50 * int(np.sum(bud[0:3])) + 50) // 100,
-                                       (50 * int(np.sum(bud[3:5])) + 50) // 100]
+    assert nxt.keep_total.tolist() == O.keep_totals(nxt, 50).tolist()
     # second pruning layer: h_prior is the first layer's kept output
     h2 = h_next + 0.3 * rng.standard_normal(h_next.shape).astype(np.float32)
     nxt2, h_next2, keep2, bud2, _ = O.progressive_step(nxt, h2, h_next, "fp32", 50)
@@ -58,3 +57,16 @@ def test_two_layer_chain_invariants():
     # the composed map sends every surviving token back to its original position in order
     orig = np.asarray(keep)[np.asarray(keep2)]
     assert np.all(np.diff(orig[0:int(nxt2.cu_seqlens[1])]) > 0)
+
+
+def test_keep_totals_hand_values():
+    """Keep totals of the next layer: keep_pct % of each sequence's remaining
+    visual tokens, halves rounded up (hand-computed)."""
+    lay = build_layout([[45], [7], [2, 3], []], 1, 1, 0)
+    # 22.5 -> 23, 3.5 -> 4, 2.5 -> 3, no visual tokens -> 0
+    assert O.keep_totals(lay, 50).tolist() == [23, 4, 3, 0]
+    lay = build_layout([[3], [1], [100]], 0, 1, 0)
+    # 0.99 -> 1, 0.33 -> 0, 33
+    assert O.keep_totals(lay, 33).tolist() == [1, 0, 33]
+    assert O.keep_totals(lay, 100).tolist() == [3, 1, 100]
+    assert O.keep_totals(lay, 0).tolist() == [0, 0, 0]
