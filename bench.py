@@ -1,17 +1,24 @@
 #!/usr/bin/env python3
 """Benchmark of the AVTP pruning layer on one MI355X.
 
-One step = one pruning layer over one batch: row statistics + column-sum
-score passes, per-image budgets, segmented top-k, and the compaction of
-hidden states, position ids and the layer's K and V.  Inputs are seeded
-synthetic tensors already resident in HBM.
+One step = one pruning layer over one batch, the four calls of the C ABI on
+one stream: avtp_score (row statistics + column-sum passes), avtp_budget,
+avtp_select and avtp_compact of hidden states, position ids and the layer's K
+and V.  Inputs are seeded synthetic tensors already resident in HBM.
 
     python bench.py [--steps K] [--warmup W] [--config 5] [--no-cpu-baseline]
+                    [--no-per-config]
 
 Prints one JSON line.  ``value`` is visual tokens processed per second for
-the whole layer; ``roofline`` describes the dominant kernel (timed live with
-HIP events on the stream the library launches on); ``cpu_baseline`` times the
-float64 CPU oracle on a bounded sample of the same workload.
+the whole layer on the headline workload (config 5); ``roofline`` describes
+the dominant kernel (timed live with HIP events on the stream the library
+launches on); ``cpu_baseline`` times the float64 CPU oracle on a bounded
+sample of the same workload.  ``per_config`` repeats the layer measurement
+on the other four workloads (time per layer, visual tokens per second, MFMA
+fraction of both score passes, HBM fraction of selection + compaction, the
+fused selection + compaction against the two calls) with an oracle time for
+each (median of 3 runs for configs 1-3 and one run for config 4 on all host
+cores, and one single-thread run for configs 1-2).
 """
 from __future__ import annotations
 
@@ -40,6 +47,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="measure only the headline workload")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB mebibytes (counter calibration)")
     return ap.parse_args()
@@ -149,26 +158,6 @@ def time_variation_and_progressive(dl, lay, hid, keep, cu_out, stream, dev, reps
             "progressive_step_us_wall": float(np.median(steps))}
 
 
-def time_select_compact(dl, scores, bud, pairs, stream, reps: int = 20) -> float:
-    """Median time of the fused selection + compaction (one launch) on this
-    step's scores, budgets and tensors."""
-    import torch
-
-    from paper_2608_26806_amd import avtp as A
-
-    def once():
-        A.select_compact(dl, scores, bud, pairs)
-
-    once()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
-    for r in range(reps):
-        ev[2 * r].record(stream)
-        once()
-        ev[2 * r + 1].record(stream)
-    torch.cuda.synchronize()
-    return float(np.median([ev[2 * r].elapsed_time(ev[2 * r + 1]) for r in range(reps)])) * 1e3
-
-
 def algorithmic_counts(lay, Hq, d, row_bytes_total):
     """Per-launch algorithmic work of each stage.
 
@@ -192,23 +181,25 @@ def algorithmic_counts(lay, Hq, d, row_bytes_total):
     return flops1, flops2, comp_bytes, sel_bytes
 
 
-def cpu_baseline(wl, nseq=3):
-    """The float64 oracle on the first `nseq` sequences of the workload (score,
-    budget, select, compaction of those sequences' hidden states)."""
-    from oracle import avtp_oracle as O
+def _oracle_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
+        return max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
     except Exception:  # noqa: BLE001
-        threads = os.cpu_count() or 1
-    lay = wl.layout
+        return os.cpu_count() or 1
+
+
+def _oracle_layer(wl, seqs):
+    """The float64 oracle's four stages on sequences `seqs` of the workload:
+    scores, budgets, selection and the compaction of those sequences' hidden
+    states.  Returns (visual tokens, text rows) processed."""
+    from oracle import avtp_oracle as O
     from paper_2608_26806_amd.workloads import Layout
-    nseq = min(nseq, lay.B)
-    t0 = time.perf_counter()
+    lay = wl.layout
     m_tot = t_tot = 0
-    for b in range(nseq):
+    for b in seqs:
         s, isum, _, _ = O.attn_scores(lay, wl.q_text, wl.k, wl.Hq, wl.Hkv, wl.softmax_scale,
-                                      wl.dtype, seqs=[b])
+                                      wl.dtype, exact_dot=(wl.cfg == 1), seqs=[b])
         i0, i1 = int(lay.cu_img[b]), int(lay.cu_img[b + 1])
         s0, s1 = int(lay.cu_seqlens[b]), int(lay.cu_seqlens[b + 1])
         ta, tb = int(lay.cu_text[b]), int(lay.cu_text[b + 1])
@@ -222,10 +213,44 @@ def cpu_baseline(wl, nseq=3):
         O.compact(keep, wl.hidden_states[s0:s1])
         m_tot += int(lay.img_len[i0:i1].sum())
         t_tot += tb - ta
+    return m_tot, t_tot
+
+
+def cpu_baseline(wl, nseq=3):
+    """The oracle on the first `nseq` sequences of the workload, all four stages."""
+    lay = wl.layout
+    nseq = min(nseq, lay.B)
+    t0 = time.perf_counter()
+    m_tot, t_tot = _oracle_layer(wl, range(nseq))
     dt = time.perf_counter() - t0
-    return {"value": m_tot / dt, "unit": "visual tokens/s", "cores": int(threads), "kind": "oracle",
+    return {"value": m_tot / dt, "unit": "visual tokens/s", "cores": int(_oracle_threads()),
+            "kind": "oracle",
             "sample": f"first {nseq} of {lay.B} sequences ({m_tot} visual tokens, {t_tot} text rows), "
                       f"all four stages, float64 numpy; {dt:.2f} s"}
+
+
+def cpu_baseline_config(wl, runs, single_thread):
+    """The oracle on the whole workload: median of `runs` runs on all host
+    cores, and (if asked) one run on one thread."""
+    lay = wl.layout
+    M = int(lay.img_len.sum())
+    times = []
+    for _ in range(runs):
+        t0 = time.perf_counter()
+        _oracle_layer(wl, range(lay.B))
+        times.append(time.perf_counter() - t0)
+    med = float(np.median(times))
+    out = {"us_per_layer": med * 1e6, "visual_tokens_per_s": M / med, "cores": int(_oracle_threads()),
+           "runs": runs, "kind": "oracle", "sample": "whole workload, all four stages"}
+    if single_thread:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            _oracle_layer(wl, range(lay.B))
+            t1 = time.perf_counter() - t0
+        out["single_thread_us_per_layer"] = t1 * 1e6
+        out["single_thread_visual_tokens_per_s"] = M / t1
+    return out
 
 
 def calibrate_copy(mib):
@@ -241,27 +266,32 @@ def calibrate_copy(mib):
     print(json.dumps({"calibration_copy_bytes": n, "dispatches": 3}))
 
 
-def main():
-    args = parse()
-    if args.calibrate_copy:
-        calibrate_copy(args.calibrate_copy)
-        return
-    if args.gpus != 1:
-        print(json.dumps({"error": "runs on one GPU only; --gpus must be 1 (the path is per "
-                                   "sequence and would shard over sequences across GPUs)"}))
-        sys.exit(2)
+def _events(stream, fn, reps):
+    """Median µs of `fn` over `reps` calls, HIP events on `stream`."""
     import torch
-    from paper_2608_26806_amd import avtp as A
-    from paper_2608_26806_amd.workloads import CONFIGS, make_workload
+    fn()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+    for r in range(reps):
+        ev[2 * r].record(stream)
+        fn()
+        ev[2 * r + 1].record(stream)
+    torch.cuda.synchronize()
+    return float(np.median([ev[2 * r].elapsed_time(ev[2 * r + 1]) for r in range(reps)])) * 1e3
 
-    if not torch.cuda.is_available():
-        print(json.dumps({"error": "no GPU visible"}))
-        sys.exit(1)
-    dev = torch.device("cuda:0")
-    t_gen = time.perf_counter()
-    wl = make_workload(args.config, payload=True)
+
+def measure_layer(wl, dev, steps, warmup):
+    """Time the pruning layer of one workload; returns (report dict, state).
+
+    The timed step is the four calls of the C ABI (avtp_score in its plain
+    two-pass form, avtp_budget, avtp_select, avtp_compact of hidden states,
+    position ids, K and V), HIP events between the calls.  Pass 1 alone
+    (avtp_row_lse: row statistics + LSE combine) is timed in a loop of its own;
+    pass 2's time is the score call's minus pass 1's."""
+    import torch
+
+    from paper_2608_26806_amd import avtp as A
+
     lay = wl.layout
-    gen_s = time.perf_counter() - t_gen
 
     def up(x):
         if wl.dtype == "bf16":
@@ -281,74 +311,123 @@ def main():
     keep = torch.empty(lay.N_out, dtype=torch.int32, device=dev)
     cu_out = torch.empty(lay.B + 1, dtype=torch.int32, device=dev)
     status = torch.zeros(lay.B, dtype=torch.int32, device=dev)
-    outs = []
     pairs = []
     for src, tdim in [(hid, 0), (pos, 1), (k, 0), (v, 0)]:
         shape = list(src.shape)
         shape[tdim] = lay.N_out
-        dst = torch.empty(shape, dtype=src.dtype, device=dev)
-        outs.append(dst)
-        pairs.append((src, dst, tdim))
+        pairs.append((src, torch.empty(shape, dtype=src.dtype, device=dev), tdim))
     row_bytes_total = sum(p[0][0].numel() * p[0].element_size() if p[2] == 0 else
                           p[0].shape[0] * p[0][0, 0].numel() * p[0].element_size() for p in pairs)
 
     stream = torch.cuda.current_stream()
-    names = ["row_lse", "score", "budget", "select", "compact"]
+    names = ["score", "budget", "select", "compact"]
+    calls = [
+        lambda: A.score_attn(dl, q, k, wl.softmax_scale, scores=scores, img_sum=isum,
+                             status=status, ws=ws),
+        lambda: A.budget(dl, isum, wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs,
+                         out=bud, status=status),
+        lambda: A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status),
+        lambda: A.compact(dl, keep, pairs),
+    ]
 
     def step(ev=None):
+        for j, c in enumerate(calls):
+            if ev is not None:
+                ev[j].record(stream)
+            c()
         if ev is not None:
-            ev[0].record(stream)
-        A.row_lse(dl, q, k, wl.softmax_scale, out=lse, ws=ws)
-        if ev is not None:
-            ev[1].record(stream)
-        A.score_attn(dl, q, k, wl.softmax_scale, row_lse=lse, scores=scores, img_sum=isum,
-                     status=status, ws=ws)
-        if ev is not None:
-            ev[2].record(stream)
-        A.budget(dl, isum, wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs, out=bud,
-                 status=status)
-        if ev is not None:
-            ev[3].record(stream)
-        A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status)
-        if ev is not None:
-            ev[4].record(stream)
-        A.compact(dl, keep, pairs)
-        if ev is not None:
-            ev[5].record(stream)
+            ev[len(calls)].record(stream)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+              for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         step(events[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per = np.array([[events[i][j].elapsed_time(events[i][j + 1]) for j in range(5)]
-                    for i in range(args.steps)])          # ms
-    layer_ms = np.array([events[i][0].elapsed_time(events[i][5]) for i in range(args.steps)])
+    per = np.array([[events[i][j].elapsed_time(events[i][j + 1]) for j in range(len(calls))]
+                    for i in range(steps)])          # ms
+    layer_ms = np.array([events[i][0].elapsed_time(events[i][len(calls)]) for i in range(steps)])
     st = status.cpu().numpy()
     if st.any():
         print(f"warning: device status flags {st.tolist()}", file=sys.stderr)
-
-    layer_sel = time_layer_selection(dl, isum, stream, dev)
-    var_prog = time_variation_and_progressive(dl, lay, hid, keep, cu_out, stream, dev)
-    fused_us = time_select_compact(dl, scores, bud, pairs, stream)
+    reps = max(steps, 10)
+    t_p1 = _events(stream, lambda: A.row_lse(dl, q, k, wl.softmax_scale, out=lse, ws=ws), reps) * 1e-3
+    fused_us = _events(stream, lambda: A.select_compact(dl, scores, bud, pairs), reps)
 
     M = int(lay.img_len.sum())
     ms_layer = float(np.median(layer_ms))
     ms = {n: float(np.mean(per[:, j])) for j, n in enumerate(names)}
     f1, f2, comp_bytes, sel_bytes = algorithmic_counts(lay, wl.Hq, wl.d, row_bytes_total)
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
-    tf1 = f1 / (ms["row_lse"] * 1e-3) / 1e12
-    tf2 = f2 / (ms["score"] * 1e-3) / 1e12
-    dom = "row_lse" if ms["row_lse"] >= ms["score"] else "score"
-    ach = tf1 if dom == "row_lse" else tf2
+    t_p2 = max(ms["score"] - t_p1, 1e-9)
+    tf1 = f1 / (t_p1 * 1e-3) / 1e12
+    tf2 = f2 / (t_p2 * 1e-3) / 1e12
     comp_gbs = comp_bytes / (ms["compact"] * 1e-3) / 1e9
     selcomp_gbs = (comp_bytes + sel_bytes) / ((ms["compact"] + ms["select"]) * 1e-3) / 1e9
-    value = M / (ms_layer * 1e-3)
+    rep = {
+        "workload": f"config {wl.cfg}: {wl.name}",
+        "dtype": wl.dtype,
+        "us_per_layer": ms_layer * 1e3,
+        "visual_tokens_per_s": M / (ms_layer * 1e-3),
+        "visual_tokens_scored_per_s": M / (ms["score"] * 1e-3),
+        "us_per_call": {n: ms[n] * 1e3 for n in names},
+        "score_passes": {
+            "pass1_us": t_p1 * 1e3, "pass2_us": t_p2 * 1e3,
+            "pass1_alg_gflop": f1 / 1e9, "pass1_tflops": tf1, "pass1_frac": tf1 / peak,
+            "pass2_alg_gflop": f2 / 1e9, "pass2_tflops": tf2, "pass2_frac": tf2 / peak,
+            "both_passes_frac": (f1 + f2) / (ms["score"] * 1e-3) / 1e12 / peak,
+            "peak_tflops": peak},
+        "roofline_compact": {"bound": "hbm", "achieved": comp_gbs, "peak": PEAK_HBM_GBS,
+                             "unit": "GB/s", "frac": comp_gbs / PEAK_HBM_GBS,
+                             "alg_bytes": comp_bytes},
+        "select_plus_compact_hbm_frac": selcomp_gbs / PEAK_HBM_GBS,
+        "select_compact_fused": {
+            "us": fused_us,
+            "hbm_frac": (comp_bytes + sel_bytes) / (fused_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+            "separate_calls_us": (ms["select"] + ms["compact"]) * 1e3},
+    }
+    state = {"dl": dl, "isum": isum, "hid": hid, "keep": keep, "cu_out": cu_out, "stream": stream,
+             "ms_layer": ms_layer, "wall": wall, "M": M, "t_p1": t_p1, "tf1": tf1, "peak": peak}
+    return rep, state
+
+
+def main():
+    args = parse()
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
+    if args.gpus != 1:
+        print(json.dumps({"error": "runs on one GPU only; --gpus must be 1 (the path is per "
+                                   "sequence and would shard over sequences across GPUs)"}))
+        sys.exit(2)
+    import torch
+    from paper_2608_26806_amd.workloads import make_workload
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    wl = make_workload(args.config, payload=True)
+    lay = wl.layout
+    gen_s = time.perf_counter() - t_gen
+
+    rep, stt = measure_layer(wl, dev, args.steps, args.warmup)
+    layer_sel = time_layer_selection(stt["dl"], stt["isum"], stt["stream"], dev)
+    var_prog = time_variation_and_progressive(stt["dl"], lay, stt["hid"], stt["keep"],
+                                              stt["cu_out"], stt["stream"], dev)
+    ms_layer = stt["ms_layer"]
+    wall = stt["wall"]
+    value = stt["M"] / (ms_layer * 1e-3)
+    ach = stt["tf1"]
+    peak = stt["peak"]
+    del stt
+    torch.cuda.empty_cache()
 
     out = {
         "metric": METRIC,
@@ -363,43 +442,47 @@ def main():
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic (seeded; shapes of the paper's LVLMs, no datasets or weights)",
-        "config": {"workload": f"config {args.config}: {CONFIGS[args.config]['name']}",
-                   "batch": lay.B, "visual_tokens": M, "text_rows": lay.T_tot,
+        "config": {"workload": rep["workload"],
+                   "batch": lay.B, "visual_tokens": int(lay.img_len.sum()), "text_rows": lay.T_tot,
                    "N_tok": lay.N_tok, "N_out": lay.N_out, "Hq": wl.Hq, "Hkv": wl.Hkv,
                    "head_dim": wl.d, "hidden": wl.hidden, "score_mode": "attn",
                    "parallelism": "none (1 GPU)"},
-        "us_per_layer": ms_layer * 1e3,
-        "us_per_call": {n: ms[n] * 1e3 for n in names},
-        "visual_tokens_scored_per_s": M / ((ms["row_lse"] + ms["score"]) * 1e-3),
+        "us_per_layer": rep["us_per_layer"],
+        "us_per_call": rep["us_per_call"],
+        "visual_tokens_scored_per_s": rep["visual_tokens_scored_per_s"],
         "roofline": {
-            "kernel": "rowstats_kernel (pass 1: row statistics; timed with its lse combine)"
-                      if dom == "row_lse" else
-                      "colsum_kernel (pass 2: column sums; timed with its finalize)",
+            "kernel": "rowstats_kernel (pass 1: row statistics; timed with its lse combine)",
             "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
             "frac": ach / peak,
-            "traffic": measured_traffic("rowstats_kernel" if dom == "row_lse" else "colsum_kernel",
-                                        f"config{args.config}",
+            "traffic": measured_traffic("rowstats_kernel", f"config{args.config}",
                                         os.path.join(HERE, "paper_2608_26806_amd", "csrc",
                                                      "score_attn.hip"))},
-        "score_passes": {
-            "pass1_alg_gflop": f1 / 1e9, "pass1_tflops": tf1, "pass1_frac": tf1 / peak,
-            "pass2_alg_gflop": f2 / 1e9, "pass2_tflops": tf2, "pass2_frac": tf2 / peak,
-            "both_passes_frac": (f1 + f2) / ((ms["row_lse"] + ms["score"]) * 1e-3) / 1e12 / peak},
-        "roofline_compact": {"bound": "hbm", "achieved": comp_gbs, "peak": PEAK_HBM_GBS,
-                             "unit": "GB/s", "frac": comp_gbs / PEAK_HBM_GBS,
-                             "alg_bytes": comp_bytes},
-        "select_plus_compact_hbm_frac": selcomp_gbs / PEAK_HBM_GBS,
-        "select_compact_fused": {
-            "us": fused_us,
-            "hbm_frac": (comp_bytes + sel_bytes) / (fused_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
-            "separate_calls_us": (ms["select"] + ms["compact"]) * 1e3},
+        "score_passes": rep["score_passes"],
+        "roofline_compact": rep["roofline_compact"],
+        "select_plus_compact_hbm_frac": rep["select_plus_compact_hbm_frac"],
+        "select_compact_fused": rep["select_compact_fused"],
         "layer_selection": layer_sel,
         "variation_and_progressive": var_prog,
         "wall_s_timed_region": wall,
         "input_generation_s": gen_s,
     }
+    per = {}
+    others = [] if args.no_per_config else [c for c in (1, 2, 3, 4) if c != args.config]
+    wls = {}
+    for c in others:
+        wc = make_workload(c, payload=True)
+        r, stc = measure_layer(wc, dev, max(5, args.steps // 2), max(2, args.warmup))
+        del stc
+        torch.cuda.empty_cache()
+        per[str(c)] = r
+        wls[c] = wc
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)
+        for c, wc in wls.items():
+            per[str(c)]["cpu_baseline"] = cpu_baseline_config(wc, runs=3 if c <= 3 else 1,
+                                                              single_thread=c <= 2)
+    if per:
+        out["per_config"] = per
     print(json.dumps(out))
 
 
