@@ -285,6 +285,29 @@ int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const f
                         int32_t *cu_out, int32_t *status, const avtp_tensor *tensors,
                         int n_tensors);
 
+/* ------------------------------------------------------------------------
+ * avtp_score_noalloc -- avtp_score for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, outputs and results as avtp_score
+ * (bit-identical: the same kernels run), but no workspace argument: the
+ * scratch space lives in a device array of AVTP_NOALLOC_MAX_WORKSPACE bytes
+ * inside the library, one per GPU, held until the process ends.  Its address
+ * on a device is looked up on the first call with that device current (a
+ * hipGetSymbolAddress, which allocates nothing); the stream must belong to the
+ * calling thread's current device.  Nothing is allocated, on any call.
+ * Returns AVTP_ERR_WORKSPACE when the layout needs more scratch than that
+ * (avtp_score_workspace_size tells how much); every other argument error as
+ * avtp_score, before any HIP call.  All calls on one GPU share its array:
+ * calls that overlap on one GPU (other streams or threads) race; calls in
+ * stream order do not.  No scratch contents need clearing between calls.
+ * ---------------------------------------------------------------------- */
+#define AVTP_NOALLOC_MAX_WORKSPACE (16 << 20) /* bytes of the library's scratch per GPU */
+int avtp_score_noalloc(avtp_stream_t stream, const avtp_layout *layout, int mode, int dtype,
+                       const void *q_text, const void *k, int Hq, int Hkv, int d,
+                       float softmax_scale, const float *row_lse, const void *h_cur,
+                       const void *h_prior, int hidden, float *scores, float *img_sum,
+                       int32_t *status);
+
 /* Human-readable name of an avtp_status value (static string). */
 const char *avtp_status_string(int status);
 

@@ -24,6 +24,7 @@ SCORE_ATTN, SCORE_VARIATION = 0, 1
 BUDGET_PROPORTIONAL, BUDGET_RAW = 0, 1
 FLAG_NAN_SCORE, FLAG_NO_TEXT_AFTER, FLAG_INFEASIBLE, FLAG_OUT_CAPACITY = 1, 2, 4, 8
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_INFEASIBLE, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4, -5
+NOALLOC_MAX_WORKSPACE = 16 << 20   # AVTP_NOALLOC_MAX_WORKSPACE of include/avtp.h
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
 
@@ -69,6 +70,8 @@ def lib() -> ctypes.CDLL:
         L.avtp_score.argtypes = [vp, LP, c_int, c_int, vp, vp, c_int, c_int, c_int, c_float, vp, vp,
                                  vp, c_int, vp, vp, vp, vp, sz]
         L.avtp_row_lse.argtypes = [vp, LP, c_int, vp, vp, c_int, c_int, c_int, c_float, vp, vp, sz]
+        L.avtp_score_noalloc.argtypes = [vp, LP, c_int, c_int, vp, vp, c_int, c_int, c_int, c_float,
+                                         vp, vp, vp, c_int, vp, vp, vp]
         L.avtp_budget.argtypes = [vp, LP, vp, c_int, c_float, c_int, c_int, c_int, vp, vp]
         L.avtp_select.argtypes = [vp, LP, vp, vp, vp, ctypes.c_int64, vp, vp]
         L.avtp_compact.argtypes = [vp, LP, vp, ctypes.c_int64, ctypes.POINTER(_Tensor), c_int]
@@ -80,7 +83,8 @@ def lib() -> ctypes.CDLL:
         L.avtp_status_string.argtypes = [c_int]
         L.avtp_status_string.restype = ctypes.c_char_p
         L.avtp_version.restype = c_int
-        for f in ("avtp_score", "avtp_row_lse", "avtp_budget", "avtp_select", "avtp_compact",
+        for f in ("avtp_score", "avtp_score_noalloc", "avtp_row_lse", "avtp_budget", "avtp_select",
+                  "avtp_compact",
                   "avtp_layer_attention", "avtp_layer_select", "avtp_pruned_layout",
                   "avtp_select_compact"):
             getattr(L, f).restype = c_int
@@ -208,6 +212,21 @@ def score_attn(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor, softmax_
                             Hkv, d, float(softmax_scale), _ptr(row_lse), None, None, 0,
                             _ptr(scores), _ptr(img_sum), _ptr(status), _ptr(ws), ws.numel()),
            "avtp_score")
+    return scores, img_sum[: dl.n_img]
+
+
+def score_attn_noalloc(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor,
+                       softmax_scale: float, scores: torch.Tensor, img_sum: torch.Tensor,
+                       row_lse: Optional[torch.Tensor] = None,
+                       status: Optional[torch.Tensor] = None, stream=None):
+    """avtp_score_noalloc in attention mode: the caller passes the outputs; the
+    library's own per-GPU scratch replaces the workspace."""
+    T, Hq, d = q_text.shape
+    Hkv = k.shape[1]
+    _check(lib().avtp_score_noalloc(_stream(stream), dl.ref(), SCORE_ATTN, dtype_code(q_text),
+                                    _ptr(q_text), _ptr(k), Hq, Hkv, d, float(softmax_scale),
+                                    _ptr(row_lse), None, None, 0, _ptr(scores), _ptr(img_sum),
+                                    _ptr(status)), "avtp_score_noalloc")
     return scores, img_sum[: dl.n_img]
 
 

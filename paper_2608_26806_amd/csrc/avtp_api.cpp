@@ -129,10 +129,15 @@ int avtp_row_lse(avtp_stream_t stream, const avtp_layout *layout, int dtype, con
                                    softmax_scale, row_lse_out, nullptr, (char *)ws));
 }
 
-int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dtype,
+}  // extern "C"
+
+namespace avtp {
+
+int score_impl(avtp_stream_t stream, const avtp_layout *layout, int mode, int dtype,
                const void *q_text, const void *k, int Hq, int Hkv, int d, float softmax_scale,
                const float *row_lse, const void *h_cur, const void *h_prior, int hidden,
-               float *scores, float *img_sum, int32_t *status, void *ws, size_t ws_bytes) {
+               float *scores, float *img_sum, int32_t *status, void *ws, size_t ws_bytes,
+               size_t *ws_need) {
   DevLayout L;
   int rc = check_layout(layout, &L);
   if (rc != AVTP_OK) return rc;
@@ -143,6 +148,10 @@ int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
     if (!h_cur || !h_prior || hidden < 1) return AVTP_ERR_INVALID_ARG;
     if (hidden % 8 != 0) return AVTP_ERR_UNSUPPORTED;
     if ((uintptr_t)h_cur % 16 || (uintptr_t)h_prior % 16) return AVTP_ERR_INVALID_ARG;
+    if (ws_need) {
+      *ws_need = variation_workspace_bytes(L);
+      return AVTP_OK;
+    }
     if (ws_bytes < variation_workspace_bytes(L)) return AVTP_ERR_WORKSPACE;
     hipError_t e = launch_variation(st, L, dtype, h_cur, h_prior, hidden, scores);
     if (e == hipSuccess) e = launch_finalize(st, L, nullptr, 0, 0, scores, img_sum, status);
@@ -155,6 +164,10 @@ int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
   if ((uintptr_t)q_text % 16 || (uintptr_t)k % 16 || (row_lse && (uintptr_t)row_lse % 4))
     return AVTP_ERR_INVALID_ARG;
   AttnPlan P = attn_plan(L, Hq, Hkv, d, dtype);
+  if (ws_need) {
+    *ws_need = P.bytes;
+    return AVTP_OK;
+  }
   if (!ws || ws_bytes < P.bytes || (uintptr_t)ws % 256) return AVTP_ERR_WORKSPACE;
   char *w = (char *)ws;
   hipError_t e = hipSuccess;
@@ -172,6 +185,18 @@ int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
     e = launch_finalize(st, L, (const float *)(w + P.off_colsum), Hq, Hkv * P.nqs, scores, img_sum,
                         status);
   return hip_status(e);
+}
+
+}  // namespace avtp
+
+extern "C" {
+
+int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dtype,
+               const void *q_text, const void *k, int Hq, int Hkv, int d, float softmax_scale,
+               const float *row_lse, const void *h_cur, const void *h_prior, int hidden,
+               float *scores, float *img_sum, int32_t *status, void *ws, size_t ws_bytes) {
+  return score_impl(stream, layout, mode, dtype, q_text, k, Hq, Hkv, d, softmax_scale, row_lse,
+                    h_cur, h_prior, hidden, scores, img_sum, status, ws, ws_bytes, nullptr);
 }
 
 int avtp_budget(avtp_stream_t stream, const avtp_layout *layout, const float *img_sum, int mode,

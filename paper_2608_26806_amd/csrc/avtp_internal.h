@@ -34,6 +34,15 @@ struct AttnPlan {
 };
 
 AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype);
+
+// avtp_score with its workspace argument.  With ws_need set, only validates
+// the arguments (returning their error, if any) and stores the workspace the
+// call needs; nothing is launched and ws is not read.
+int score_impl(avtp_stream_t stream, const avtp_layout *layout, int mode, int dtype,
+               const void *q_text, const void *k, int Hq, int Hkv, int d, float softmax_scale,
+               const float *row_lse, const void *h_cur, const void *h_prior, int hidden,
+               float *scores, float *img_sum, int32_t *status, void *ws, size_t ws_bytes,
+               size_t *ws_need);
 size_t variation_workspace_bytes(const DevLayout &L);
 
 // Pass 1 and the combine: the row LSE (natural log) into row_lse and, if

@@ -175,3 +175,27 @@ def test_select_compact_arguments_rejected_on_host():
     assert lib.avtp_select_compact(None, dl.ref(), p, p, p, 1, p, None, t, 0) == A.ERR_INVALID_ARG  # capacity
     assert lib.avtp_select_compact(None, dl.ref(), p, p, p, 100, p, None, t, 9) == A.ERR_UNSUPPORTED
     assert lib.avtp_select_compact(None, dl.ref(), p, p, p, 100, p, None, t, 1) == A.ERR_INVALID_ARG  # null src
+
+
+def test_noalloc_rejects_oversize_and_bad_args_on_the_host():
+    """avtp_score_noalloc checks every argument, and that the layout fits its
+    scratch, before any HIP call (so this runs without a GPU)."""
+    lib = A.lib()
+    buf = torch.zeros(1 << 16, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    # one 200k-token image, 64 key heads: the column-sum planes alone need 51 MB
+    big = _dl(build_layout([[200000]], 0, 8, 10))
+    need = A.score_workspace_bytes(big, A.SCORE_ATTN, A.BF16, 64, 64, 128)
+    assert need > A.NOALLOC_MAX_WORKSPACE
+    rc = lib.avtp_score_noalloc(None, big.ref(), A.SCORE_ATTN, A.BF16, p, p, 64, 64, 128, 0.1,
+                                None, None, None, 0, p, p, None)
+    assert rc == A.ERR_WORKSPACE
+    small = _dl()
+    for args, want in [((4, 2, 96), A.ERR_UNSUPPORTED), ((4, 3, 128), A.ERR_INVALID_ARG)]:
+        Hq, Hkv, d = args
+        rc = lib.avtp_score_noalloc(None, small.ref(), A.SCORE_ATTN, A.BF16, p, p, Hq, Hkv, d, 0.1,
+                                    None, None, None, 0, p, p, None)
+        assert rc == want
+    rc = lib.avtp_score_noalloc(None, small.ref(), A.SCORE_ATTN, A.BF16, p, p, 4, 2, 128, 0.1,
+                                None, None, None, 0, None, p, None)
+    assert rc == A.ERR_INVALID_ARG
