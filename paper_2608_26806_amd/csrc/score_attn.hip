@@ -219,7 +219,7 @@ __device__ inline void interleave_mfma_valu() {
 // k-steps (none if they were read before the tile), then per k-step the NT
 // MFMAs of the step, each followed by up to V VALU ops working on the
 // previous tile, then the LDS read of the fragment PF steps ahead.
-template <int NS, int NT, int V, int LEAD>
+template <int NS, int NT, int V, int LEAD, bool NX = false>
 __device__ inline void interleave_tile() {
   constexpr int PF = NS < 3 ? NS : 3;
   if (LEAD > 0) __builtin_amdgcn_sched_group_barrier(0x100, LEAD, 0);  // DS read
@@ -230,7 +230,8 @@ __device__ inline void interleave_tile() {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // VALU
     }
-    if (s + PF < NS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    // the fragment PF steps ahead: of this tile, or (NX) of the next one
+    if (s + PF < NS || NX) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
   }
 }
 
@@ -390,22 +391,27 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   for (int i = 0; i < 2 * NT; ++i) acc[i] = f32x16{};
   constexpr int kNone = 1 << 30;  // pend_kb of an empty pending tile: no lane sees it
   int pend_kb = kNone;
-  constexpr int kAllOrNone = 1, kPerElem = 2;
+  constexpr int kAll = 0, kAllOrNone = 1, kPerElem = 2;
+  using All = std::integral_constant<int, kAll>;
   using AllOrNone = std::integral_constant<int, kAllOrNone>;
   using PerElem = std::integral_constant<int, kPerElem>;
 
   // One key tile: MFMAs of the tile at buf row `lrow` into the sets of
   // parity P (if MF), and the exp2 sums of the pending tile (sets of parity
-  // P^1).  Mode M: kAllOrNone (every lane sees all or none of the pending
-  // tile) or kPerElem (per-element mask).
+  // P^1).  Mode M: kAll (every lane sees the whole pending tile), kAllOrNone
+  // (every lane sees all or none of it) or kPerElem (per-element mask).
+  // With NX the tile's last PF k-steps read the first PF fragments of the
+  // next tile (at lrow + 32) into pf, for that tile's PRE.
   constexpr int PF = NS < 3 ? NS : 3;  // key fragments are read PF k-steps ahead of their MFMAs
   frag pf[PF];                          // a tile's first PF fragments, if read before it (PRE)
-  auto tile = [&](const char *buf, int lrow, auto par_tag, auto mode_tag, auto mf_tag, auto pre_tag)
-      __attribute__((always_inline)) {
+  using NoNext = std::false_type;
+  auto tile = [&](const char *buf, int lrow, auto par_tag, auto mode_tag, auto mf_tag, auto pre_tag,
+                  auto nx_tag) __attribute__((always_inline)) {
     constexpr int P = decltype(par_tag)::value;
     constexpr int M = decltype(mode_tag)::value;
     constexpr bool MF = decltype(mf_tag)::value;
     constexpr bool PRE = decltype(pre_tag)::value;
+    constexpr bool NX = decltype(nx_tag)::value;
     constexpr int CS = P * NT, PS = (P ^ 1) * NT;
     // per-element limit (kPerElem); in kAllOrNone a lane sees the whole
     // pending tile unless its row precedes it, and only lanes that see it
@@ -434,6 +440,9 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
       if (MF) {
         if (s + PF < NS)
           av[s + PF] = load_frag<frag>(buf + swz_off<T, D>(lrow + col, (s + PF) * 2 * E + hi * E));
+        else if (NX)
+          pf[s + PF - NS] =
+              load_frag<frag>(buf + swz_off<T, D>(lrow + 32 + col, (s + PF - NS) * 2 * E + hi * E));
 #pragma unroll
         for (int qi = 0; qi < NT; ++qi) acc[CS + qi] = MM::run(av[s], qf[qi][s], acc[CS + qi]);
       }
@@ -451,7 +460,7 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
     }
     if (MF)
       interleave_tile<NS, NT, ((M == kPerElem ? 64 : 40) / NS > 0 ? (M == kPerElem ? 64 : 40) / NS : 1),
-                      PRE ? 0 : PF>();
+                      PRE ? 0 : PF, NX>();
     float t[NT];
     bool bad = false;
 #pragma unroll
@@ -499,7 +508,30 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
     wait_vmem();
     __syncthreads();  // stage st is in LDS; every wave is done with the other buffer
     if (st + 1 < nstage) issue_stage(ks + KS, nxt);
-    if ((st + 1) * TPS <= ntw) {
+    // every lane sees every pending tile of the stage (the previous stage's
+    // last tile and this stage's first TPS-1): no per-tile checks, and each
+    // tile reads the next one's first fragments
+    bool allvis = false;
+    if ((st + 1) * TPS <= ntw && pend_kb != kNone) {
+#pragma unroll
+      for (int s = 0; s < PF; ++s) pf[s] = load_frag<frag>(buf + swz_off<T, D>(col, s * 2 * E + hi * E));
+      bool part = false;
+#pragma unroll
+      for (int qi = 0; qi < NT; ++qi) part = part || qrel[qi] < ks + (TPS - 1) * 32 - 1;
+      allvis = __ballot(part) == 0ull;
+    }
+    if (allvis) {
+      using P0_ = std::integral_constant<int, 0>;
+      using P1_ = std::integral_constant<int, 1>;
+      using Yes = std::true_type;
+      tile(buf, 0, P0_{}, All{}, Yes{}, Yes{}, Yes{});
+      tile(buf, 32, P1_{}, All{}, Yes{}, Yes{}, Yes{});
+      if constexpr (TPS == 4) {
+        tile(buf, 64, P0_{}, All{}, Yes{}, Yes{}, Yes{});
+        tile(buf, 96, P1_{}, All{}, Yes{}, Yes{}, NoNext{});
+      }
+      pend_kb = ks + (TPS - 1) * 32;
+    } else if ((st + 1) * TPS <= ntw) {
       // every tile of the stage is this wave's: no per-tile bounds
       auto one = [&](auto kt_tag) __attribute__((always_inline)) {
         constexpr int KT = decltype(kt_tag)::value;
@@ -514,9 +546,9 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
 #pragma unroll
         for (int qi = 0; qi < NT; ++qi) part = part || (unsigned)(qrel[qi] - pend_kb) < 31u;
         if (__ballot(part) == 0ull)
-          tile(buf, KT * 32, par_tag{}, AllOrNone{}, std::true_type{}, std::true_type{});
+          tile(buf, KT * 32, par_tag{}, AllOrNone{}, std::true_type{}, std::true_type{}, NoNext{});
         else
-          tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{}, std::true_type{});
+          tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{}, std::true_type{}, NoNext{});
         pend_kb = ks + KT * 32;
       };
       static_assert(TPS == 2 || TPS == 4, "one stage is two or four key tiles");
@@ -532,10 +564,10 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
         constexpr int KT = decltype(kt_tag)::value;
         using par_tag = std::integral_constant<int, KT & 1>;
         if (st * TPS + KT < ntw) {
-          tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{}, std::false_type{});
+          tile(buf, KT * 32, par_tag{}, PerElem{}, std::true_type{}, std::false_type{}, NoNext{});
           pend_kb = ks + KT * 32;
         } else if (st * TPS + KT == ntw) {
-          tile(buf, 0, par_tag{}, PerElem{}, std::false_type{}, std::false_type{});
+          tile(buf, 0, par_tag{}, PerElem{}, std::false_type{}, std::false_type{}, NoNext{});
           pend_kb = kNone;
         }
       };
@@ -553,7 +585,7 @@ __global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Ar
   }
   if (!active) return;
   // with a whole number of stages the pending tile is the last (odd) one
-  if (ntw > 0 && ntw % TPS == 0) tile(smA, 0, P0{}, PerElem{}, std::false_type{}, std::false_type{});
+  if (ntw > 0 && ntw % TPS == 0) tile(smA, 0, P0{}, PerElem{}, std::false_type{}, std::false_type{}, NoNext{});
 
   // merge the two half-waves (same query column, disjoint keys) and store
 #pragma unroll
