@@ -16,7 +16,9 @@ import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libavtp.so")
+# AVTP_LIBRARY names another build of the same library (e.g. the host-sanitized
+# one the CPU tests check the validation layer with)
+LIB_PATH = os.environ.get("AVTP_LIBRARY") or os.path.join(_HERE, "libavtp.so")
 HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "avtp.h")
 
 BF16, FP32 = 0, 1

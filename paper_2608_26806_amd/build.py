@@ -55,5 +55,33 @@ def build(verbose: bool = True) -> str:
     return LIB
 
 
+def build_host_sanitized(out_path: str) -> str:
+    """A copy of the library whose host validation layer (avtp_api.cpp) is
+    built with AddressSanitizer and UndefinedBehaviorSanitizer (host code
+    only; the kernels are the regular objects).  Used by the CPU tests, which
+    load it with the ASan runtime preloaded.  Builds the regular objects first
+    if they are missing."""
+    objdir = os.path.join(HERE, "_build")
+    objs = [os.path.join(objdir, os.path.splitext(x)[0] + ".o") for x in SOURCES]
+    if not all(os.path.exists(o) for o in objs):
+        build(verbose=False)
+    san_obj = out_path + ".api.o"
+    cmd = [HIPCC, "-O1", "-g", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+           "-fno-omit-frame-pointer",
+           "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+           "-Xarch_host", "-fno-sanitize-recover=undefined",
+           "-c", os.path.join(CSRC, "avtp_api.cpp"), "-o", san_obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("sanitized build of avtp_api.cpp failed:\n" + r.stdout + r.stderr)
+    others = [o for o in objs if not o.endswith(os.sep + "avtp_api.o")]
+    r = subprocess.run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *others, san_obj,
+                        "-o", out_path], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
+    os.remove(san_obj)
+    return out_path
+
+
 if __name__ == "__main__":
     build()
