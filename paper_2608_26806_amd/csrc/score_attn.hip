@@ -1151,11 +1151,13 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   // Split the query rows of pass 2 only when its grid would not fill the
   // chip twice over (512 blocks): a block pays for loading its keys and for
   // filling its pipeline, so fewer, longer blocks are faster; keep at least
-  // 512 rows (four stages) per split.
+  // 512 rows (four stages) per split.  A grid of less than one block per CU
+  // is latency-bound instead: there a split may go down to one stage.
   {
     const long long base2 = (long long)L.B * Hkv * P.nkb;
     long long nq = base2 >= 512 ? 1 : (512 + base2 - 1) / base2;
-    const long long cap = (P.rows_max + 511) / 512;
+    const long long min_rows = base2 < 256 ? kStage : 512;
+    const long long cap = (P.rows_max + min_rows - 1) / min_rows;
     if (nq > cap) nq = cap;
     P.nqs = nq < 1 ? 1 : (int)nq;
   }

@@ -130,7 +130,7 @@ def test_score_with_supplied_lse_skips_pass1(cfg):
 def _plan_query_splits(lay, Hq, Hkv, d, row_bytes):
     """Query splits of pass 2 by the launch plan's rule: split only when the
     (sequence, key head, 4*NT*32-key block) grid is under 512 blocks, keeping
-    at least 512 rows per split."""
+    at least 512 rows per split (128 when the grid is under 256 blocks)."""
     nt = max(1, min(4, 96 // (row_bytes // 8)))
     kpb = 4 * nt * 32
     L = int(np.max(np.diff(lay.cu_seqlens)))
@@ -138,7 +138,8 @@ def _plan_query_splits(lay, Hq, Hkv, d, row_bytes):
     nkb = -(-L // kpb)
     base = lay.B * Hkv * nkb
     nq = 1 if base >= 512 else -(-512 // base)
-    return max(1, min(nq, -(-(Hq // Hkv) * T // 512)))
+    min_rows = 128 if base < 256 else 512
+    return max(1, min(nq, -(-(Hq // Hkv) * T // min_rows)))
 
 
 SHAPES = {
