@@ -357,7 +357,15 @@ def measure_layer(wl, dev, steps, warmup):
         print(f"warning: device status flags {st.tolist()}", file=sys.stderr)
     reps = max(steps, 10)
     t_p1 = _events(stream, lambda: A.row_lse(dl, q, k, wl.softmax_scale, out=lse, ws=ws), reps) * 1e-3
+    # the fused call and the two separate calls, timed the same way (events
+    # around each call, or around the pair)
     fused_us = _events(stream, lambda: A.select_compact(dl, scores, bud, pairs), reps)
+
+    def _sep():
+        A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status)
+        A.compact(dl, keep, pairs)
+
+    sep_us = _events(stream, _sep, reps)
 
     M = int(lay.img_len.sum())
     ms_layer = float(np.median(layer_ms))
@@ -389,7 +397,7 @@ def measure_layer(wl, dev, steps, warmup):
         "select_compact_fused": {
             "us": fused_us,
             "hbm_frac": (comp_bytes + sel_bytes) / (fused_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
-            "separate_calls_us": (ms["select"] + ms["compact"]) * 1e3},
+            "separate_calls_us": sep_us},
     }
     state = {"dl": dl, "isum": isum, "hid": hid, "keep": keep, "cu_out": cu_out, "stream": stream,
              "ms_layer": ms_layer, "wall": wall, "M": M, "t_p1": t_p1, "tf1": tf1, "peak": peak}

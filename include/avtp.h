@@ -273,12 +273,16 @@ int avtp_layer_select(avtp_stream_t stream, const float *A, int L, int N, int k,
 
 /* ------------------------------------------------------------------------
  * avtp_select_compact -- avtp_select followed by avtp_compact of the same
- * tensors to n_out = T_tot + sum(keep_total) rows, in one launch (for the
- * small configurations, where the launches and the selection's latency
- * dominate).  Same arguments and outputs as the two calls; the kept rows and
- * keep_idx are bit-identical to theirs.  Every image is handled by several
- * blocks that each redo its selection and copy an interleaved share of its
- * output rows, so no block waits for another.
+ * tensors to n_out = T_tot + sum(keep_total) rows (the pruned subsequence of
+ * Method, "Visual Token Pruning", gathered in one call).  Same arguments and
+ * outputs as the two calls; the kept rows and keep_idx are bit-identical to
+ * theirs.  When the compaction moves at most 32 MiB (reads plus writes) it is
+ * one launch, for the small configurations where launches and the
+ * selection's latency dominate: every image is handled by several blocks
+ * that each redo its selection and copy an interleaved share of its output
+ * rows, so no block waits for another.  Above that the two kernels run back
+ * to back (one block's copies cannot start before its selection ends, so the
+ * one-launch form is slower there).
  * ---------------------------------------------------------------------- */
 int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const float *scores,
                         const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,

@@ -76,6 +76,9 @@ int check_attn_args(int dtype, int Hq, int Hkv, int d) {
   return AVTP_OK;
 }
 
+// avtp_select_compact: bytes moved above which it runs the two kernels
+constexpr int64_t kFusedMaxBytes = 32ll << 20;
+
 int64_t n_out_of(const avtp_layout *lay) {
   int64_t n = lay->T_tot;
   for (int b = 0; b < lay->B; ++b) n += lay->h_keep_total[b];
@@ -316,8 +319,23 @@ int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const f
   if (keep_capacity < need || (need > 0 && !keep_idx)) return AVTP_ERR_INVALID_ARG;
   rc = check_tensors(L, need, tensors, n_tensors);
   if (rc != AVTP_OK) return rc;
-  return hip_status(launch_select_compact((hipStream_t)stream, L, scores, budget, keep_idx,
-                                          keep_capacity, cu_out, status, need, tensors, n_tensors));
+  // One launch pays where launches and the selection's latency dominate (few
+  // bytes to move).  Every block of the fused kernel runs its image's
+  // selection before it copies, so the copies cannot start before the
+  // selections end; with many bytes to move the two kernels back to back are
+  // faster (measured: config 2, 15 MB: one launch 27 us, two 31 us; config
+  // 3, 240 MB: 39 us and 34 us), and are used instead.
+  int64_t moved = 0;
+  for (int i = 0; i < n_tensors; ++i) moved += 2 * need * tensors[i].row_bytes * tensors[i].planes;
+  hipStream_t st = (hipStream_t)stream;
+  if (moved > kFusedMaxBytes) {
+    hipError_t e = launch_select(st, L, scores, budget, keep_idx, keep_capacity, cu_out, status);
+    if (e == hipSuccess && need > 0 && n_tensors > 0)
+      e = launch_compact(st, L, keep_idx, need, tensors, n_tensors);
+    return hip_status(e);
+  }
+  return hip_status(launch_select_compact(st, L, scores, budget, keep_idx, keep_capacity, cu_out,
+                                          status, need, tensors, n_tensors));
 }
 
 }  // extern "C"
