@@ -32,11 +32,12 @@ int check_layout(const avtp_layout *lay, DevLayout *out) {
   const int32_t *cs = lay->h_cu_seqlens, *ci = lay->h_cu_img, *ct = lay->h_cu_text;
   if (cs[0] != 0 || ci[0] != 0 || ct[0] != 0) return AVTP_ERR_INVALID_ARG;
   if (cs[B] != N || ci[B] != n_img || ct[B] != T) return AVTP_ERR_INVALID_ARG;
-  int max_seq = 0, max_text = 0, max_img = 0;
+  int max_seq = 0, max_text = 0, max_img = 0, max_ips = 0;
   for (int b = 0; b < B; ++b) {
     const int s0 = cs[b], s1 = cs[b + 1];
     if (s1 < s0 || ci[b + 1] < ci[b] || ct[b + 1] < ct[b]) return AVTP_ERR_INVALID_ARG;
     if (ci[b + 1] - ci[b] > AVTP_MAX_IMAGES_PER_SEQ) return AVTP_ERR_UNSUPPORTED;
+    max_ips = std::max(max_ips, ci[b + 1] - ci[b]);
     int64_t covered = ct[b + 1] - ct[b];
     int prev_end = s0;
     for (int i = ci[b]; i < ci[b + 1]; ++i) {
@@ -62,8 +63,9 @@ int check_layout(const avtp_layout *lay, DevLayout *out) {
     max_text = std::max(max_text, ct[b + 1] - ct[b]);
   }
   if (out) {
-    *out = DevLayout{B, n_img, N, T, max_seq, max_text, max_img, lay->cu_seqlens, lay->img_start,
-                     lay->img_len, lay->cu_img, lay->text_pos, lay->cu_text, lay->keep_total};
+    *out = DevLayout{B,        n_img,        N,           T,           max_seq,        max_text,
+                     max_img,  max_ips,      lay->cu_seqlens, lay->img_start, lay->img_len,
+                     lay->cu_img, lay->text_pos, lay->cu_text, lay->keep_total};
   }
   return AVTP_OK;
 }

@@ -15,6 +15,7 @@ namespace avtp {
 struct DevLayout {
   int B, n_img, N_tok, T_tot;
   int max_seqlen, max_text, max_img_len;
+  int max_img_per_seq;
   const int32_t *cu_seqlens, *img_start, *img_len, *cu_img, *text_pos, *cu_text, *keep_total;
 };
 

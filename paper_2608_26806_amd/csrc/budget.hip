@@ -60,14 +60,19 @@ __device__ double image_weight(int n, long long M, float s32, double S, bool goo
   return w;
 }
 
-constexpr int kThreads = 256;  // one thread per image (kMaxImg)
+// One thread per image: blocks of 256 threads, or a single wave of 64 when
+// no sequence has more than 16 images (then every block-wide reduction is a
+// wave butterfly, with no LDS round trip or barrier; with more images the
+// four waves' share of the breakpoint sums pays more).
+constexpr int kThreads = 256;
 static_assert(kMaxImg <= kThreads, "one thread per image");
 
 // Block-wide sums: wave butterflies, then the four wave partials in LDS.
-template <typename T>
+template <int NTH, typename T>
 __device__ inline T block_sum(T v, T *sh) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if (NTH == 64) return v;
   if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
   __syncthreads();
   const T r = sh[0] + sh[1] + sh[2] + sh[3];
@@ -77,7 +82,7 @@ __device__ inline T block_sum(T v, T *sh) {
 
 // Block-wide extreme of fractions num/den (den > 0) among the threads with
 // ok set: the smallest (MIN) or the largest.  Returns ok = false if none.
-template <bool MIN>
+template <bool MIN, int NTH>
 __device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, uint64_t *shn,
                                       uint64_t *shd, int *sho) {
   auto better = [](uint64_t an, uint64_t ad, uint64_t bn, uint64_t bd) {
@@ -93,6 +98,7 @@ __device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, ui
       ok = true;
     }
   }
+  if (NTH == 64) return;
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
     shn[w] = num;
@@ -111,7 +117,8 @@ __device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, ui
   __syncthreads();
 }
 
-__global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restrict__ img_sum,
+template <int NTH>
+__global__ __launch_bounds__(NTH) void budget_kernel(const float *__restrict__ img_sum,
                                                           const int32_t *__restrict__ img_len,
                                                           const int32_t *__restrict__ cu_img,
                                                           const int32_t *__restrict__ keep_total,
@@ -119,7 +126,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
                                                           int floor_abs, int32_t *__restrict__ budget,
                                                           int32_t *__restrict__ status) {
   __shared__ uint64_t W[kMaxImg], rem[kMaxImg];
-  __shared__ uint64_t fpart[kThreads];  // partial f of a breakpoint, one per thread
+  __shared__ uint64_t fpart[NTH];  // partial f of a breakpoint, one per thread
   __shared__ int32_t lo[kMaxImg], hi[kMaxImg];
   __shared__ float sv[kMaxImg];
   __shared__ long long red_i[4];
@@ -147,9 +154,10 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
     hi[tid] = (int32_t)h;
     sv[tid] = s32;
   }
-  const long long M = block_sum(n, red_i);
-  const long long slo = block_sum(l, red_i);
-  const long long shi = block_sum(h, red_i);
+  const long long M = block_sum<NTH>(n, red_i);
+  const long long slo = block_sum<NTH>(l, red_i);
+  const long long shi = block_sum<NTH>(h, red_i);
+  if (NTH == 64) __syncthreads();  // sv is read by thread 0 below
   if (tid == 0) {  // the image sum, in image order (it fixes the weights)
     double S = 0.0;
     for (int i = 0; i < m; ++i) S = S + (double)sv[i];
@@ -164,9 +172,11 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
   double wmax = w;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) wmax = fmax(wmax, __shfl_xor(wmax, off));
-  if ((tid & 63) == 0) red_d[tid >> 6] = wmax;
-  __syncthreads();
-  wmax = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
+  if (NTH > 64) {
+    if ((tid & 63) == 0) red_d[tid >> 6] = wmax;
+    __syncthreads();
+    wmax = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
+  }
   uint64_t Wi = 0;
   if (mine) {
     if (n > 0) {
@@ -220,9 +230,9 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
     hp = hp || tp;
   };
   const int nbp = 2 * m;
-  const int np = nbp <= kThreads / 4 ? 4 : (nbp <= kThreads / 2 ? 2 : 1);  // parts; block-uniform
+  const int np = nbp <= NTH / 4 ? 4 : (nbp <= NTH / 2 ? 2 : 1);  // parts; block-uniform
   if (np > 1) {
-    const int KB = kThreads / np;  // >= nbp
+    const int KB = NTH / np;  // >= nbp
     const int k = tid % KB, part = tid / KB;
     const int per = (m + np - 1) / np, j0 = min(m, part * per), j1 = min(m, j0 + per);
     bool ok = false;
@@ -243,15 +253,15 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
       keep_ext(f, num, den);
     }
   } else {
-    for (int k = tid; k < nbp; k += kThreads) {
+    for (int k = tid; k < nbp; k += NTH) {
       const int i = k < m ? k : k - m;
       if (W[i] == 0) continue;
       const uint64_t num = (uint64_t)(k < m ? lo[i] : hi[i]), den = W[i];
       keep_ext(partial_f(num, den, 0, m), num, den);
     }
   }
-  block_frac_ext<true>(bn, bd, hn, ext_n, ext_d, ext_o);
-  block_frac_ext<false>(pn, pd, hp, ext_n, ext_d, ext_o);
+  block_frac_ext<true, NTH>(bn, bd, hn, ext_n, ext_d, ext_o);
+  block_frac_ext<false, NTH>(pn, pd, hp, ext_n, ext_d, ext_o);
 
   // classify the images on the segment (prev, next]: pinned at lo, at hi, or free
   int32_t kk = 0;
@@ -271,8 +281,8 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
       freeW = Wi;
     }
   }
-  const uint64_t P = (uint64_t)K - block_sum(pinned, red_u);
-  const uint64_t Q = block_sum(freeW, red_u);
+  const uint64_t P = (uint64_t)K - block_sum<NTH>(pinned, red_u);
+  const uint64_t Q = block_sum<NTH>(freeW, red_u);
   uint64_t ri = 0;
   if (fr) {
     const uint64_t num = P * Wi;
@@ -280,7 +290,8 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
     ri = num % Q;
   }
   if (mine) rem[tid] = ri;
-  const long long D = K - block_sum((long long)kk, red_i);  // the units left to hand out
+  if (NTH == 64) __syncthreads();  // rem is read by every lane below
+  const long long D = K - block_sum<NTH>((long long)kk, red_i);  // the units left to hand out
   // largest remainders first, lowest image index among equal ones
   if (mine) {
     long long rank = 0;
@@ -294,9 +305,14 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(const float *__restric
 hipError_t launch_budget(hipStream_t st, const DevLayout &L, const float *img_sum, int mode,
                          float alpha, int lo_permille, int hi_permille, int floor_abs,
                          int32_t *budget, int32_t *status) {
-  hipLaunchKernelGGL(budget_kernel, dim3(L.B), dim3(kThreads), 0, st, img_sum, L.img_len, L.cu_img,
-                     L.keep_total, mode, alpha, lo_permille, hi_permille, floor_abs, budget,
-                     status);
+  if (L.max_img_per_seq <= 16)
+    hipLaunchKernelGGL(budget_kernel<64>, dim3(L.B), dim3(64), 0, st, img_sum, L.img_len, L.cu_img,
+                       L.keep_total, mode, alpha, lo_permille, hi_permille, floor_abs, budget,
+                       status);
+  else
+    hipLaunchKernelGGL(budget_kernel<kThreads>, dim3(L.B), dim3(kThreads), 0, st, img_sum,
+                       L.img_len, L.cu_img, L.keep_total, mode, alpha, lo_permille, hi_permille,
+                       floor_abs, budget, status);
   return hipGetLastError();
 }
 

@@ -1126,13 +1126,18 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   P.rows_max = P.G * L.max_text;
   P.nqb = (P.rows_max + rows_per_block - 1) / rows_per_block;
   if (P.nqb < 1) P.nqb = 1;
-  // split keys so that pass 1 launches about 2048 blocks (8 per CU)
+  // split keys so that pass 1 launches about 2048 blocks (8 per CU); chunks
+  // of at least two stages, or one on a grid of less than one block per CU,
+  // where a block's latency is what counts
   const long long base = (long long)L.B * Hkv * P.nqb;
   long long want = (2048 + base - 1) / base;
   if (want < 1) want = 1;
   long long kc = (L.max_seqlen + want - 1) / want;
   kc = ((kc + kStage - 1) / kStage) * kStage;
-  if (kc < 256) kc = 256;
+  if (kc < 2 * kStage1) {
+    const long long two = (L.max_seqlen + 2 * kStage1 - 1) / (2 * kStage1);  // chunks of two stages
+    kc = base * two < 256 ? (kc < kStage1 ? kStage1 : kc) : 2 * kStage1;
+  }
   P.kchunk = (int)kc;
   P.nkc = (L.max_seqlen + P.kchunk - 1) / P.kchunk;
   if (P.nkc < 1) P.nkc = 1;

@@ -237,11 +237,13 @@ def test_budget_bit_exact_on_same_image_sums():
         assert not status.any()
 
 
-def test_budget_mixed_image_counts_one_launch():
+@pytest.mark.parametrize("counts", [(10, 50, 150), (1, 10, 3, 16)])
+def test_budget_mixed_image_counts_one_launch(counts):
     # sequences of 10, 50 and 150 images in one launch: their blocks take the
-    # three ways of splitting the breakpoint sums
-    rng = np.random.default_rng(19)
-    seqs = [[int(x) for x in rng.integers(1, 300, size=m)] for m in (10, 50, 150)]
+    # three ways of splitting the breakpoint sums; with at most 16 images per
+    # sequence the kernel runs one wave per sequence
+    rng = np.random.default_rng(19 + len(counts))
+    seqs = [[int(x) for x in rng.integers(1, 300, size=m)] for m in counts]
     lay = build_layout(seqs, 2, 3, 0)
     keeps = []
     for n in seqs:
@@ -251,7 +253,7 @@ def test_budget_mixed_image_counts_one_launch():
     lay.keep_total[:] = keeps
     dl = A.DeviceLayout(lay)
     S = (rng.lognormal(0.0, 1.5, size=lay.n_img) * lay.img_len / 100).astype(np.float32)
-    say("[budget] mixed image counts 10/50/150")
+    say(f"[budget] mixed image counts {counts}")
     status = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
     g = A.budget(dl, torch.from_numpy(S).cuda(), 1.0, 50, 950, 8, status=status).cpu().numpy()
     assert np.array_equal(g, O.budget(lay, S, 1.0, 50, 950, 8))
