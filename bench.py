@@ -189,10 +189,12 @@ def _oracle_threads():
         return os.cpu_count() or 1
 
 
-def _oracle_layer(wl, seqs):
+def _oracle_layer(wl, seqs, keep_out=None):
     """The float64 oracle's four stages on sequences `seqs` of the workload:
     scores, budgets, selection and the compaction of those sequences' hidden
-    states.  Returns (visual tokens, text rows) processed."""
+    states.  Returns (visual tokens, text rows) processed; if keep_out is a
+    dict, it receives each sequence's oracle outputs (for the parity check,
+    after the timing)."""
     from oracle import avtp_oracle as O
     from paper_2608_26806_amd.workloads import Layout
     lay = wl.layout
@@ -210,18 +212,64 @@ def _oracle_layer(wl, seqs):
         bud = O.budget(sub, isum[i0:i1].astype(np.float32), wl.alpha, wl.lo_permille,
                        wl.hi_permille, wl.floor_abs)
         keep, _ = O.select(sub, s[s0:s1].astype(np.float32), bud)
-        O.compact(keep, wl.hidden_states[s0:s1])
+        hid = O.compact(keep, wl.hidden_states[s0:s1])
         m_tot += int(lay.img_len[i0:i1].sum())
         t_tot += tb - ta
+        if keep_out is not None:
+            keep_out[b] = {"scores": s[s0:s1], "isum": isum[i0:i1], "budget": bud, "keep": keep,
+                           "hidden": hid, "sub": sub}
     return m_tot, t_tot
 
 
-def cpu_baseline(wl, nseq=3):
+def parity_verdict(wl, gpu, orc):
+    """The GPU layer's outputs against the oracle's on the sequences the oracle
+    ran (gpu: host copies of scores, image sums, budgets, keep_idx, cu_out and
+    the compacted hidden states).  Scores and image sums: largest relative
+    error (tolerance 2e-3 for bf16, 1e-5 for fp32); budgets: equal to the
+    oracle's on the oracle's own sums and on the GPU's; kept tokens: equal
+    outside each image's threshold band; compaction: bit-exact given the
+    GPU's kept indices."""
+    from oracle import avtp_oracle as O
+    lay = wl.layout
+    tol = 2e-3 if wl.dtype == "bf16" else 1e-5
+    err_s = err_i = 0.0
+    bud_eq = bud_gpu_eq = comp_eq = True
+    outside = 0
+    for b, o in orc.items():
+        s0, s1 = int(lay.cu_seqlens[b]), int(lay.cu_seqlens[b + 1])
+        i0, i1 = int(lay.cu_img[b]), int(lay.cu_img[b + 1])
+        sub = o["sub"]
+        vis = sub.visual_mask()
+        sg = gpu["scores"][s0:s1]
+        err_s = max(err_s, float(np.max(np.abs(sg[vis] - o["scores"][vis]) / o["scores"][vis])))
+        ig = gpu["isum"][i0:i1]
+        err_i = max(err_i, float(np.max(np.abs(ig - o["isum"]) / o["isum"])))
+        bg = gpu["budget"][i0:i1]
+        bud_eq &= bool(np.array_equal(bg, o["budget"]))
+        bud_gpu_eq &= bool(np.array_equal(bg, O.budget(sub, ig, wl.alpha, wl.lo_permille,
+                                                       wl.hi_permille, wl.floor_abs)))
+        kg = gpu["keep"][gpu["cu_out"][b]:gpu["cu_out"][b + 1]] - s0
+        for j in set(kg.tolist()) ^ set(o["keep"].tolist()):
+            i = int(np.searchsorted(sub.img_start, j, side="right") - 1)
+            st, n = int(sub.img_start[i]), int(sub.img_len[i])
+            k = int(o["budget"][i])
+            theta = np.sort(o["scores"][st:st + n])[::-1][max(k - 1, 0)]
+            outside += int(not (st <= j < st + n and abs(o["scores"][j] - theta) <= tol * theta))
+        comp_eq &= bool(np.array_equal(gpu["hidden"][gpu["cu_out"][b]:gpu["cu_out"][b + 1]],
+                                       wl.hidden_states[s0:s1][kg]))
+    ok = err_s <= tol and err_i <= tol and bud_eq and bud_gpu_eq and outside == 0 and comp_eq
+    return {"sequences": sorted(int(b) for b in orc), "tolerance": tol,
+            "scores_max_rel_err": err_s, "img_sum_max_rel_err": err_i,
+            "budgets_equal_oracle": bud_eq, "budgets_equal_on_gpu_sums": bud_gpu_eq,
+            "kept_outside_threshold_band": outside, "compaction_bit_exact": comp_eq, "ok": ok}
+
+
+def cpu_baseline(wl, nseq=3, keep_out=None):
     """The oracle on the first `nseq` sequences of the workload, all four stages."""
     lay = wl.layout
     nseq = min(nseq, lay.B)
     t0 = time.perf_counter()
-    m_tot, t_tot = _oracle_layer(wl, range(nseq))
+    m_tot, t_tot = _oracle_layer(wl, range(nseq), keep_out)
     dt = time.perf_counter() - t0
     return {"value": m_tot / dt, "unit": "visual tokens/s", "cores": int(_oracle_threads()),
             "kind": "oracle",
@@ -229,15 +277,15 @@ def cpu_baseline(wl, nseq=3):
                       f"all four stages, float64 numpy; {dt:.2f} s"}
 
 
-def cpu_baseline_config(wl, runs, single_thread):
+def cpu_baseline_config(wl, runs, single_thread, keep_out=None):
     """The oracle on the whole workload: median of `runs` runs on all host
     cores, and (if asked) one run on one thread."""
     lay = wl.layout
     M = int(lay.img_len.sum())
     times = []
-    for _ in range(runs):
+    for r in range(runs):
         t0 = time.perf_counter()
-        _oracle_layer(wl, range(lay.B))
+        _oracle_layer(wl, range(lay.B), keep_out if r == 0 else None)
         times.append(time.perf_counter() - t0)
     med = float(np.median(times))
     out = {"us_per_layer": med * 1e6, "visual_tokens_per_s": M / med, "cores": int(_oracle_threads()),
@@ -399,9 +447,23 @@ def measure_layer(wl, dev, steps, warmup):
             "hbm_frac": (comp_bytes + sel_bytes) / (fused_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
             "separate_calls_us": sep_us},
     }
+    torch.cuda.synchronize()
+    host = {"scores": scores.cpu().numpy(), "isum": isum[:lay.n_img].cpu().numpy(),
+            "budget": bud[:lay.n_img].cpu().numpy(), "keep": keep.cpu().numpy(),
+            "cu_out": cu_out.cpu().numpy(), "hidden": _host_bits(pairs[0][1])}
     state = {"dl": dl, "isum": isum, "hid": hid, "keep": keep, "cu_out": cu_out, "stream": stream,
-             "ms_layer": ms_layer, "wall": wall, "M": M, "t_p1": t_p1, "tf1": tf1, "peak": peak}
+             "ms_layer": ms_layer, "wall": wall, "M": M, "t_p1": t_p1, "tf1": tf1, "peak": peak,
+             "host": host}
     return rep, state
+
+
+def _host_bits(t):
+    """Device tensor -> numpy array of its raw bits (bf16 as uint16)."""
+    import torch
+    t = t.detach().contiguous().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
 
 
 def main():
@@ -431,6 +493,7 @@ def main():
                                               stt["cu_out"], stt["stream"], dev)
     ms_layer = stt["ms_layer"]
     wall = stt["wall"]
+    host5 = stt["host"]
     value = stt["M"] / (ms_layer * 1e-3)
     ach = stt["tf1"]
     peak = stt["peak"]
@@ -476,19 +539,24 @@ def main():
     }
     per = {}
     others = [] if args.no_per_config else [c for c in (1, 2, 3, 4) if c != args.config]
-    wls = {}
+    wls, hosts = {}, {}
     for c in others:
         wc = make_workload(c, payload=True)
         r, stc = measure_layer(wc, dev, max(5, args.steps // 2), max(2, args.warmup))
+        hosts[c] = stc["host"]
         del stc
         torch.cuda.empty_cache()
         per[str(c)] = r
         wls[c] = wc
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl)
+        orc = {}
+        out["cpu_baseline"] = cpu_baseline(wl, keep_out=orc)
+        out["parity"] = parity_verdict(wl, host5, orc)
         for c, wc in wls.items():
+            orc = {}
             per[str(c)]["cpu_baseline"] = cpu_baseline_config(wc, runs=3 if c <= 3 else 1,
-                                                              single_thread=c <= 2)
+                                                              single_thread=c <= 2, keep_out=orc)
+            per[str(c)]["parity"] = parity_verdict(wc, hosts[c], orc)
     if per:
         out["per_config"] = per
     print(json.dumps(out))
