@@ -415,6 +415,17 @@ def measure_layer(wl, dev, steps, warmup):
 
     sep_us = _events(stream, _sep, reps)
 
+    # the layer with the row LSE supplied by the caller (the layer's own
+    # attention hands it over): pass 2 only, then budget, select, compact
+    def _layer_lse():
+        A.score_attn(dl, q, k, wl.softmax_scale, row_lse=lse, scores=scores, img_sum=isum,
+                     status=status, ws=ws)
+        calls[1]()
+        calls[2]()
+        calls[3]()
+
+    lse_layer_us = _events(stream, _layer_lse, reps)
+
     M = int(lay.img_len.sum())
     ms_layer = float(np.median(layer_ms))
     ms = {n: float(np.mean(per[:, j])) for j, n in enumerate(names)}
@@ -442,6 +453,7 @@ def measure_layer(wl, dev, steps, warmup):
                              "unit": "GB/s", "frac": comp_gbs / PEAK_HBM_GBS,
                              "alg_bytes": comp_bytes},
         "select_plus_compact_hbm_frac": selcomp_gbs / PEAK_HBM_GBS,
+        "layer_with_supplied_lse_us": lse_layer_us,
         "select_compact_fused": {
             "us": fused_us,
             "hbm_frac": (comp_bytes + sel_bytes) / (fused_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
@@ -531,6 +543,7 @@ def main():
         "score_passes": rep["score_passes"],
         "roofline_compact": rep["roofline_compact"],
         "select_plus_compact_hbm_frac": rep["select_plus_compact_hbm_frac"],
+        "layer_with_supplied_lse_us": rep["layer_with_supplied_lse_us"],
         "select_compact_fused": rep["select_compact_fused"],
         "layer_selection": layer_sel,
         "variation_and_progressive": var_prog,

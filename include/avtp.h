@@ -21,8 +21,9 @@
  *     to AVTP_ERR_HIP.
  *   - Data-dependent conditions found on the device are OR-ed into the
  *     optional per-sequence status word (int32 [B], caller zero-fills it).
- *   - Outputs must not alias inputs.  No global mutable state: calls on
- *     different streams with different buffers may run concurrently.
+ *   - Outputs must not alias inputs.  No global mutable state (except the
+ *     per-GPU scratch of avtp_score_noalloc, below): calls on different
+ *     streams with different buffers may run concurrently.
  */
 #ifndef AVTP_H
 #define AVTP_H

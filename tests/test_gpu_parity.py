@@ -381,15 +381,16 @@ def test_compact_out_of_range_index_leaves_row():
 
 
 # ------------------------------------------------------------------ end to end
-def _budget_margin_ok(lay, wl, isum_o, rel, trials=8):
+def _budget_margin_ok(lay, wl, isum_o, rel, trials=8, singles=True):
     """The oracle's budgets stay the same when the oracle's image sums move by
     `rel` (relative): every image alone, both signs, and `trials` random joint
     moves.  With `rel` above the GPU's largest image-sum error this shows the
-    end-to-end budget equality does not rest on luck."""
-    bud = lambda v: O.budget(lay, v.astype(np.float32), wl.alpha, wl.lo_permille, wl.hi_permille,
-                             wl.floor_abs)
+    end-to-end budget equality does not rest on luck.  wl: a workload, or a
+    tuple (alpha, lo_permille, hi_permille, floor_abs)."""
+    args = (wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs) if hasattr(wl, "alpha") else wl
+    bud = lambda v: O.budget(lay, v.astype(np.float32), *args)
     base = bud(isum_o)
-    for i in range(lay.n_img):
+    for i in (range(lay.n_img) if singles else ()):
         for sgn in (1.0, -1.0):
             v = isum_o.copy()
             v[i] *= 1.0 + sgn * rel
@@ -547,6 +548,48 @@ def test_variation_parity(cfg, batch):
 
 
 # ------------------------------------------------------------------ edge layouts
+def test_end_to_end_most_images_per_sequence():
+    """256 images per sequence (the most the library takes), 1 to 12 tokens
+    each, two sequences: scores and image sums against the oracle, budgets
+    bit-exact on the GPU's sums and equal to the oracle chain's, selection and
+    compaction bit-exact."""
+    rng = np.random.default_rng(256)
+    seqs = [[int(x) for x in rng.integers(1, 13, size=256)] for _ in range(2)]
+    lay = build_layout(seqs, 1, 5, 40)
+    Hq, Hkv, d = 8, 2, 64
+    q32 = rng.standard_normal((lay.T_tot, Hq, d)).astype(np.float32)
+    k32 = rng.standard_normal((lay.N_tok, Hkv, d)).astype(np.float32)
+    k32[lay.visual_mask()] *= np.repeat(np.exp(0.7 * rng.standard_normal(lay.n_img)), lay.img_len)[:, None, None].astype(np.float32)
+    qb, kb = f32_to_bf16_bits(q32), f32_to_bf16_bits(k32)
+    hid = f32_to_bf16_bits(rng.standard_normal((lay.N_tok, 96)).astype(np.float32))
+    say(f"[end to end] 256 images per sequence: N_tok={lay.N_tok} n_img={lay.n_img}")
+    dl = A.DeviceLayout(lay)
+    status = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+    s_g, isum_g = A.score_attn(dl, to_dev(qb, "bf16"), to_dev(kb, "bf16"), d ** -0.5, status=status)
+    bud_g = A.budget(dl, isum_g, 1.0, 50, 950, 0, status=status)
+    keep_g, cu_g = A.select(dl, s_g, bud_g, status=status)
+    (hid_out,) = A.compact_new(dl, keep_g, [(to_dev(hid, "bf16"), 0)])
+    torch.cuda.synchronize()
+    assert not status.cpu().numpy().any()
+    s_g, isum_g, bud_g = s_g.cpu().numpy(), isum_g.cpu().numpy(), bud_g.cpu().numpy()
+    keep_g, cu_g = keep_g.cpu().numpy(), cu_g.cpu().numpy()
+    s_o, isum_o, _, _ = O.attn_scores(lay, qb, kb, Hq, Hkv, d ** -0.5, "bf16")
+    vis = lay.visual_mask()
+    assert_rel(s_g[vis], s_o[vis], TOL["bf16"], "scores")
+    assert_rel(isum_g, isum_o, TOL["bf16"], "image sums")
+    assert np.array_equal(bud_g, O.budget(lay, isum_g, 1.0, 50, 950, 0))
+    bud_o = O.budget(lay, isum_o.astype(np.float32), 1.0, 50, 950, 0)
+    assert np.flatnonzero(bud_g != bud_o).tolist() == []
+    err = float(np.max(np.abs(isum_g - isum_o) / np.abs(isum_o)))
+    # (joint moves only: one oracle allocation of 512 images takes over a second)
+    assert _budget_margin_ok(lay, (1.0, 50, 950, 0), isum_o, 4.0 * err, trials=6, singles=False)
+    keep_s, cu_s = O.select(lay, s_g, bud_g)
+    assert np.array_equal(keep_g, keep_s) and np.array_equal(cu_g, cu_s)
+    keep_o, _ = O.select(lay, s_o.astype(np.float32), bud_o)
+    kept_sets_match(lay, keep_g, keep_o, s_o, bud_o, TOL["bf16"])
+    assert np.array_equal(to_host_bits(hid_out), O.compact(keep_g, hid))
+
+
 def test_edge_layout_ragged_empty_and_no_text_after():
     """Empty image, single-token image, ragged lengths, a sequence without
     images, and an image with no text row after it (flagged, scores 0)."""
