@@ -49,6 +49,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-per-config", action="store_true",
                     help="measure only the headline workload")
+    ap.add_argument("--sustain-s", type=float, default=3.0, metavar="S",
+                    help="after the timed steps, run each score pass back to back for S seconds and "
+                         "report its steady-state time (0: off)")
+    ap.add_argument("--sustain-only", action="store_true",
+                    help="only the sustained loops of the headline workload (e.g. for power sampling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB mebibytes (counter calibration)")
     return ap.parse_args()
@@ -80,6 +85,36 @@ def measured_traffic(kernel, workload, src_path):
         return (float(kv["fetch_kib"]) * 1024 / float(kv["copy_read"])
                 + float(kv["write_kib"]) * 1024 / float(kv["copy_write"]))
     return None
+
+
+def time_sustained(st, seconds: float) -> dict:
+    """Each score pass run back to back for `seconds` (after the timed steps):
+    the steady-state time per call once the GPU's power controller has
+    settled (the first tens of ms of a run are a transient).  Pass 1 is
+    avtp_row_lse; pass 2 is avtp_score given that LSE (pass 2, LSE
+    conversion, finalize).  Reported beside the timed steps, never as
+    `value`."""
+    import torch
+
+    from paper_2608_26806_amd import avtp as A
+
+    dl, q, k, lse, ws, wl = st["dl"], st["q"], st["k"], st["lse"], st["ws"], st["wl"]
+    scores, isum = st["scores"], st["isum"]
+    out = {}
+    for name, fn in [("pass1_us", lambda: A.row_lse(dl, q, k, wl.softmax_scale, out=lse, ws=ws)),
+                     ("pass2_us", lambda: A.score_attn(dl, q, k, wl.softmax_scale, row_lse=lse,
+                                                       scores=scores, img_sum=isum, ws=ws))]:
+        fn()
+        torch.cuda.synchronize()
+        n, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(20):
+                fn()
+            torch.cuda.synchronize()
+            n += 20
+        out[name] = (time.perf_counter() - t0) / n * 1e6
+        out[name.replace("_us", "_calls")] = n
+    return out
 
 
 def time_layer_selection(dl, isum, stream, dev, reps: int = 50) -> dict:
@@ -465,7 +500,8 @@ def measure_layer(wl, dev, steps, warmup):
             "cu_out": cu_out.cpu().numpy(), "hidden": _host_bits(pairs[0][1])}
     state = {"dl": dl, "isum": isum, "hid": hid, "keep": keep, "cu_out": cu_out, "stream": stream,
              "ms_layer": ms_layer, "wall": wall, "M": M, "t_p1": t_p1, "tf1": tf1, "peak": peak,
-             "host": host}
+             "host": host, "q": q, "k": k, "lse": lse, "ws": ws, "wl": wl, "scores": scores,
+             "f12": (f1, f2)}
     return rep, state
 
 
@@ -488,6 +524,7 @@ def main():
                                    "sequence and would shard over sequences across GPUs)"}))
         sys.exit(2)
     import torch
+    from paper_2608_26806_amd import avtp as A
     from paper_2608_26806_amd.workloads import make_workload
 
     if not torch.cuda.is_available():
@@ -499,7 +536,31 @@ def main():
     lay = wl.layout
     gen_s = time.perf_counter() - t_gen
 
+    if args.sustain_only:
+        dl = A.DeviceLayout(lay, device=dev)
+        up = (lambda x: torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16)
+              .to(dev)) if wl.dtype == "bf16" else (lambda x: torch.from_numpy(
+                  np.ascontiguousarray(x, dtype=np.float32)).to(dev))
+        dt = A.BF16 if wl.dtype == "bf16" else A.FP32
+        stt = {"dl": dl, "q": up(wl.q_text), "k": up(wl.k), "wl": wl,
+               "lse": torch.empty((wl.Hq, lay.T_tot), dtype=torch.float32, device=dev),
+               "ws": A.alloc_workspace(A.score_workspace_bytes(dl, A.SCORE_ATTN, dt, wl.Hq, wl.Hkv,
+                                                               wl.d), dev),
+               "scores": torch.empty(lay.N_tok, dtype=torch.float32, device=dev),
+               "isum": torch.empty(max(1, lay.n_img), dtype=torch.float32, device=dev)}
+        print(json.dumps({"workload": f"config {args.config}",
+                          "sustained": time_sustained(stt, max(args.sustain_s, 1.0))}))
+        return
     rep, stt = measure_layer(wl, dev, args.steps, args.warmup)
+    sustained = None
+    if args.sustain_s > 0:
+        sustained = time_sustained(stt, args.sustain_s)
+        f1, f2 = stt["f12"]
+        pk = stt["peak"]
+        sustained["pass1_frac"] = f1 / (sustained["pass1_us"] * 1e-6) / 1e12 / pk
+        sustained["both_passes_frac"] = (f1 + f2) / ((sustained["pass1_us"] + sustained["pass2_us"])
+                                                     * 1e-6) / 1e12 / pk
+        sustained["seconds_per_pass"] = args.sustain_s
     layer_sel = time_layer_selection(stt["dl"], stt["isum"], stt["stream"], dev)
     var_prog = time_variation_and_progressive(stt["dl"], lay, stt["hid"], stt["keep"],
                                               stt["cu_out"], stt["stream"], dev)
@@ -541,6 +602,7 @@ def main():
                                         os.path.join(HERE, "paper_2608_26806_amd", "csrc",
                                                      "score_attn.hip"))},
         "score_passes": rep["score_passes"],
+        "score_passes_sustained": sustained,
         "roofline_compact": rep["roofline_compact"],
         "select_plus_compact_hbm_frac": rep["select_plus_compact_hbm_frac"],
         "layer_with_supplied_lse_us": rep["layer_with_supplied_lse_us"],
