@@ -365,11 +365,14 @@ def _events(stream, fn, reps):
 def measure_layer(wl, dev, steps, warmup):
     """Time the pruning layer of one workload; returns (report dict, state).
 
-    The timed step is the four calls of the C ABI (avtp_score in its plain
-    two-pass form, avtp_budget, avtp_select, avtp_compact of hidden states,
-    position ids, K and V), HIP events between the calls.  Pass 1 alone
-    (avtp_row_lse: row statistics + LSE combine) is timed in a loop of its own;
-    pass 2's time is the score call's minus pass 1's."""
+    The timed step is two calls of the C ABI: avtp_score in its plain
+    two-pass form, then avtp_budget_select_compact (budgets, selection and
+    the compaction of hidden states, position ids, K and V), HIP events
+    between the calls.  The same layer as four calls (avtp_score, avtp_budget,
+    avtp_select, avtp_compact) is timed after it, events between the calls,
+    for the per-stage breakdown.  Pass 1 alone (avtp_row_lse: row statistics
+    + LSE combine) is timed in a loop of its own; pass 2's time is the score
+    call's minus pass 1's."""
     import torch
 
     from paper_2608_26806_amd import avtp as A
@@ -403,38 +406,51 @@ def measure_layer(wl, dev, steps, warmup):
                           p[0].shape[0] * p[0][0, 0].numel() * p[0].element_size() for p in pairs)
 
     stream = torch.cuda.current_stream()
+    score_call = lambda: A.score_attn(dl, q, k, wl.softmax_scale, scores=scores, img_sum=isum,
+                                      status=status, ws=ws)
+    bargs = (wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs)
+    calls = [  # the timed step
+        score_call,
+        lambda: A.budget_select_compact(dl, isum, scores, pairs, *bargs, budget_out=bud,
+                                        keep_idx=keep, cu_out=cu_out, status=status),
+    ]
     names = ["score", "budget", "select", "compact"]
-    calls = [
-        lambda: A.score_attn(dl, q, k, wl.softmax_scale, scores=scores, img_sum=isum,
-                             status=status, ws=ws),
-        lambda: A.budget(dl, isum, wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs,
-                         out=bud, status=status),
+    calls4 = [  # the same layer as four calls
+        score_call,
+        lambda: A.budget(dl, isum, *bargs, out=bud, status=status),
         lambda: A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status),
         lambda: A.compact(dl, keep, pairs),
     ]
 
-    def step(ev=None):
-        for j, c in enumerate(calls):
+    def step(cs, ev=None):
+        for j, c in enumerate(cs):
             if ev is not None:
                 ev[j].record(stream)
             c()
         if ev is not None:
-            ev[len(calls)].record(stream)
+            ev[len(cs)].record(stream)
+
+    def run(cs, n):
+        """n steps of the calls cs, events between the calls; returns the
+        per-call times (ms, one row per step), the step times and the wall
+        time."""
+        events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(cs) + 1)]
+                  for _ in range(n)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(n):
+            step(cs, events[i])
+        torch.cuda.synchronize()
+        w = time.perf_counter() - t0
+        per_ = np.array([[events[i][j].elapsed_time(events[i][j + 1]) for j in range(len(cs))]
+                         for i in range(n)])
+        return per_, np.array([events[i][0].elapsed_time(events[i][len(cs)]) for i in range(n)]), w
 
     for _ in range(warmup):
-        step()
+        step(calls)
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
-              for _ in range(steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(steps):
-        step(events[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    per = np.array([[events[i][j].elapsed_time(events[i][j + 1]) for j in range(len(calls))]
-                    for i in range(steps)])          # ms
-    layer_ms = np.array([events[i][0].elapsed_time(events[i][len(calls)]) for i in range(steps)])
+    per2, layer_ms, wall = run(calls, steps)           # the timed steps
+    per, layer4_ms, _ = run(calls4, max(steps, 10))    # the four-call breakdown
     st = status.cpu().numpy()
     if st.any():
         print(f"warning: device status flags {st.tolist()}", file=sys.stderr)
@@ -456,17 +472,17 @@ def measure_layer(wl, dev, steps, warmup):
         A.score_attn(dl, q, k, wl.softmax_scale, row_lse=lse, scores=scores, img_sum=isum,
                      status=status, ws=ws)
         calls[1]()
-        calls[2]()
-        calls[3]()
 
     lse_layer_us = _events(stream, _layer_lse, reps)
 
     M = int(lay.img_len.sum())
     ms_layer = float(np.median(layer_ms))
     ms = {n: float(np.mean(per[:, j])) for j, n in enumerate(names)}
+    ms_score = float(np.mean(per2[:, 0]))
+    ms_prune = float(np.mean(per2[:, 1]))
     f1, f2, comp_bytes, sel_bytes = algorithmic_counts(lay, wl.Hq, wl.d, row_bytes_total)
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
-    t_p2 = max(ms["score"] - t_p1, 1e-9)
+    t_p2 = max(ms_score - t_p1, 1e-9)
     tf1 = f1 / (t_p1 * 1e-3) / 1e12
     tf2 = f2 / (t_p2 * 1e-3) / 1e12
     comp_gbs = comp_bytes / (ms["compact"] * 1e-3) / 1e9
@@ -476,13 +492,15 @@ def measure_layer(wl, dev, steps, warmup):
         "dtype": wl.dtype,
         "us_per_layer": ms_layer * 1e3,
         "visual_tokens_per_s": M / (ms_layer * 1e-3),
-        "visual_tokens_scored_per_s": M / (ms["score"] * 1e-3),
-        "us_per_call": {n: ms[n] * 1e3 for n in names},
+        "visual_tokens_scored_per_s": M / (ms_score * 1e-3),
+        "us_per_call": {"score": ms_score * 1e3, "budget_select_compact": ms_prune * 1e3},
+        "four_calls": {"us_per_layer": float(np.median(layer4_ms)) * 1e3,
+                       "us_per_call": {n: ms[n] * 1e3 for n in names}},
         "score_passes": {
             "pass1_us": t_p1 * 1e3, "pass2_us": t_p2 * 1e3,
             "pass1_alg_gflop": f1 / 1e9, "pass1_tflops": tf1, "pass1_frac": tf1 / peak,
             "pass2_alg_gflop": f2 / 1e9, "pass2_tflops": tf2, "pass2_frac": tf2 / peak,
-            "both_passes_frac": (f1 + f2) / (ms["score"] * 1e-3) / 1e12 / peak,
+            "both_passes_frac": (f1 + f2) / (ms_score * 1e-3) / 1e12 / peak,
             "peak_tflops": peak},
         "roofline_compact": {"bound": "hbm", "achieved": comp_gbs, "peak": PEAK_HBM_GBS,
                              "unit": "GB/s", "frac": comp_gbs / PEAK_HBM_GBS,

@@ -291,6 +291,29 @@ int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const f
                         int n_tensors);
 
 /* ------------------------------------------------------------------------
+ * avtp_budget_select_compact -- avtp_budget, then avtp_select_compact: the
+ * per-image budgets of Sec. 3.3.3 (adaptive keep ratio, appendix clamp on
+ * alpha), the top-budget selection of every image and the gather of the
+ * pruned subsequence (Method, "Visual Token Pruning"), in one call.
+ * Arguments: those of avtp_budget (img_sum, mode, alpha, lo/hi permille,
+ * floor_abs; budget[n_img] is written) followed by those of
+ * avtp_select_compact.  Every output (budget, keep_idx, cu_out, the compacted
+ * tensors, status flags) is bit-identical to the separate calls'.  Errors: as
+ * the separate calls, all checked on the host before any launch, including
+ * AVTP_ERR_INFEASIBLE.  While no sequence has more than 64 images, the
+ * selection blocks each run the budget rule for their own sequence (the
+ * same integer arithmetic as the budget kernel), so no budget launch is
+ * needed: one launch in all when the compaction moves at most 32 MiB, else
+ * the selection and the compaction kernels.  With more images per sequence
+ * the budget kernel runs first.
+ * ---------------------------------------------------------------------- */
+int avtp_budget_select_compact(avtp_stream_t stream, const avtp_layout *layout,
+                               const float *img_sum, int mode, float alpha, int lo_permille,
+                               int hi_permille, int floor_abs, const float *scores, int32_t *budget,
+                               int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out,
+                               int32_t *status, const avtp_tensor *tensors, int n_tensors);
+
+/* ------------------------------------------------------------------------
  * avtp_score_noalloc -- avtp_score for callers that cannot allocate device
  * memory (code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc).  Same arguments, outputs and results as avtp_score

@@ -80,6 +80,9 @@ def lib() -> ctypes.CDLL:
         L.avtp_pruned_layout.argtypes = [vp, LP, vp, vp, vp, vp, vp, vp, vp, vp]
         L.avtp_select_compact.argtypes = [vp, LP, vp, vp, vp, ctypes.c_int64, vp, vp,
                                           ctypes.POINTER(_Tensor), c_int]
+        L.avtp_budget_select_compact.argtypes = [vp, LP, vp, c_int, ctypes.c_float, c_int, c_int,
+                                                 c_int, vp, vp, vp, ctypes.c_int64, vp, vp,
+                                                 ctypes.POINTER(_Tensor), c_int]
         L.avtp_layer_attention.argtypes = [vp, LP, vp, vp]
         L.avtp_layer_select.argtypes = [vp, vp, c_int, c_int, c_int, vp, vp]
         L.avtp_status_string.argtypes = [c_int]
@@ -88,7 +91,7 @@ def lib() -> ctypes.CDLL:
         for f in ("avtp_score", "avtp_score_noalloc", "avtp_row_lse", "avtp_budget", "avtp_select",
                   "avtp_compact",
                   "avtp_layer_attention", "avtp_layer_select", "avtp_pruned_layout",
-                  "avtp_select_compact"):
+                  "avtp_select_compact", "avtp_budget_select_compact"):
             getattr(L, f).restype = c_int
         _lib = L
     return _lib
@@ -321,6 +324,31 @@ def select_compact(dl: DeviceLayout, scores: torch.Tensor, budget_: torch.Tensor
                                      _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out), _ptr(status),
                                      arr, len(descs)), "avtp_select_compact")
     return keep_idx[: dl.N_out], cu_out
+
+
+def budget_select_compact(dl: DeviceLayout, img_sum: torch.Tensor, scores: torch.Tensor,
+                          pairs: Sequence, alpha: float = 1.0, lo_permille: int = 50,
+                          hi_permille: int = 950, floor_abs: int = 0,
+                          mode: int = BUDGET_PROPORTIONAL, budget_out: Optional[torch.Tensor] = None,
+                          keep_idx: Optional[torch.Tensor] = None,
+                          cu_out: Optional[torch.Tensor] = None,
+                          status: Optional[torch.Tensor] = None, stream=None):
+    """avtp_budget followed by avtp_select_compact, in one call; pairs as for
+    compact.  Returns (budget, keep_idx, cu_out)."""
+    dev = scores.device
+    if budget_out is None:
+        budget_out = torch.empty(max(1, dl.n_img), dtype=torch.int32, device=dev)
+    if keep_idx is None:
+        keep_idx = torch.empty(max(1, dl.N_out), dtype=torch.int32, device=dev)
+    if cu_out is None:
+        cu_out = torch.empty(dl.B + 1, dtype=torch.int32, device=dev)
+    descs = [tensor_desc(p[0], p[1], p[2] if len(p) > 2 else 0) for p in pairs]
+    arr = (_Tensor * max(1, len(descs)))(*descs)
+    _check(lib().avtp_budget_select_compact(
+        _stream(stream), dl.ref(), _ptr(img_sum), mode, float(alpha), lo_permille, hi_permille,
+        floor_abs, _ptr(scores), _ptr(budget_out), _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out),
+        _ptr(status), arr, len(descs)), "avtp_budget_select_compact")
+    return budget_out[: dl.n_img], keep_idx[: dl.N_out], cu_out
 
 
 def compact_new(dl: DeviceLayout, keep_idx: torch.Tensor, srcs: Sequence, stream=None):

@@ -80,6 +80,9 @@ int check_attn_args(int dtype, int Hq, int Hkv, int d) {
 
 // avtp_select_compact: bytes moved above which it runs the two kernels
 constexpr int64_t kFusedMaxBytes = 32ll << 20;
+// avtp_budget_select_compact: most images per sequence for which the
+// selection blocks run the budget rule themselves
+constexpr int kInBlockBudgetMaxImages = 64;
 
 int64_t n_out_of(const avtp_layout *lay) {
   int64_t n = lay->T_tot;
@@ -204,12 +207,11 @@ int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
                     h_cur, h_prior, hidden, scores, img_sum, status, ws, ws_bytes, nullptr);
 }
 
-int avtp_budget(avtp_stream_t stream, const avtp_layout *layout, const float *img_sum, int mode,
-                float alpha, int lo_permille, int hi_permille, int floor_abs, int32_t *budget,
-                int32_t *status) {
-  DevLayout L;
-  int rc = check_layout(layout, &L);
-  if (rc != AVTP_OK) return rc;
+// The budget rule's arguments, and that every sequence's keep total lies
+// between the sums of its images' bounds.
+static int check_budget(const avtp_layout *layout, const DevLayout &L, const float *img_sum,
+                        int mode, float alpha, int lo_permille, int hi_permille, int floor_abs,
+                        const int32_t *budget) {
   if (mode != AVTP_BUDGET_PROPORTIONAL && mode != AVTP_BUDGET_RAW) return AVTP_ERR_INVALID_ARG;
   if (!(alpha >= 0.f && alpha <= 32.f)) return AVTP_ERR_INVALID_ARG;
   if (lo_permille < 0 || hi_permille > 1000 || lo_permille > hi_permille || floor_abs < 0)
@@ -228,6 +230,17 @@ int avtp_budget(avtp_stream_t stream, const avtp_layout *layout, const float *im
     const int64_t K = layout->h_keep_total[b];
     if (K < slo || K > shi) return AVTP_ERR_INFEASIBLE;
   }
+  return AVTP_OK;
+}
+
+int avtp_budget(avtp_stream_t stream, const avtp_layout *layout, const float *img_sum, int mode,
+                float alpha, int lo_permille, int hi_permille, int floor_abs, int32_t *budget,
+                int32_t *status) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  rc = check_budget(layout, L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget);
+  if (rc != AVTP_OK) return rc;
   if (L.n_img == 0) return AVTP_OK;
   return hip_status(launch_budget((hipStream_t)stream, L, img_sum, mode, alpha, lo_permille,
                                   hi_permille, floor_abs, budget, status));
@@ -309,6 +322,13 @@ int avtp_compact(avtp_stream_t stream, const avtp_layout *layout, const int32_t 
   return hip_status(launch_compact((hipStream_t)stream, L, keep_idx, n_out, tensors, n_tensors));
 }
 
+// bytes a compaction of n_out rows of these tensors reads and writes
+static int64_t bytes_moved(int64_t n_out, const avtp_tensor *tensors, int n_tensors) {
+  int64_t moved = 0;
+  for (int i = 0; i < n_tensors; ++i) moved += 2 * n_out * tensors[i].row_bytes * tensors[i].planes;
+  return moved;
+}
+
 int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const float *scores,
                         const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
                         int32_t *cu_out, int32_t *status, const avtp_tensor *tensors,
@@ -327,8 +347,7 @@ int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const f
   // selections end; with many bytes to move the two kernels back to back are
   // faster (measured: config 2, 15 MB: one launch 27 us, two 31 us; config
   // 3, 240 MB: 39 us and 34 us), and are used instead.
-  int64_t moved = 0;
-  for (int i = 0; i < n_tensors; ++i) moved += 2 * need * tensors[i].row_bytes * tensors[i].planes;
+  const int64_t moved = bytes_moved(need, tensors, n_tensors);
   hipStream_t st = (hipStream_t)stream;
   if (moved > kFusedMaxBytes) {
     hipError_t e = launch_select(st, L, scores, budget, keep_idx, keep_capacity, cu_out, status);
@@ -338,6 +357,48 @@ int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const f
   }
   return hip_status(launch_select_compact(st, L, scores, budget, keep_idx, keep_capacity, cu_out,
                                           status, need, tensors, n_tensors));
+}
+
+int avtp_budget_select_compact(avtp_stream_t stream, const avtp_layout *layout,
+                               const float *img_sum, int mode, float alpha, int lo_permille,
+                               int hi_permille, int floor_abs, const float *scores, int32_t *budget,
+                               int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out,
+                               int32_t *status, const avtp_tensor *tensors, int n_tensors) {
+  DevLayout L;
+  int rc = check_layout(layout, &L);
+  if (rc != AVTP_OK) return rc;
+  rc = check_budget(layout, L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget);
+  if (rc != AVTP_OK) return rc;
+  if (!scores || !cu_out) return AVTP_ERR_INVALID_ARG;
+  const int64_t need = n_out_of(layout);
+  if (keep_capacity < need || (need > 0 && !keep_idx)) return AVTP_ERR_INVALID_ARG;
+  rc = check_tensors(L, need, tensors, n_tensors);
+  if (rc != AVTP_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  // Every selection block runs the budget rule for its own sequence, which
+  // costs less than a launch while sequences have few images; with many, the
+  // budget kernel runs once per sequence first.
+  if (L.max_img_per_seq > kInBlockBudgetMaxImages) {
+    hipError_t e = hipSuccess;
+    if (L.n_img > 0)
+      e = launch_budget(st, L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget,
+                        status);
+    if (e != hipSuccess) return hip_status(e);
+    return avtp_select_compact(stream, layout, scores, budget, keep_idx, keep_capacity, cu_out,
+                               status, tensors, n_tensors);
+  }
+  if (bytes_moved(need, tensors, n_tensors) > kFusedMaxBytes) {
+    hipError_t e = launch_budget_select(st, L, img_sum, mode, alpha, lo_permille, hi_permille,
+                                        floor_abs, scores, budget, keep_idx, keep_capacity, cu_out,
+                                        status);
+    if (e == hipSuccess && need > 0 && n_tensors > 0)
+      e = launch_compact(st, L, keep_idx, need, tensors, n_tensors);
+    return hip_status(e);
+  }
+  return hip_status(launch_budget_select_compact(st, L, img_sum, mode, alpha, lo_permille,
+                                                 hi_permille, floor_abs, scores, budget, keep_idx,
+                                                 keep_capacity, cu_out, status, need, tensors,
+                                                 n_tensors));
 }
 
 }  // extern "C"

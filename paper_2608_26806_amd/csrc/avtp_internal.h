@@ -78,6 +78,20 @@ hipError_t launch_select_compact(hipStream_t stream, const DevLayout &L, const f
                                  const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
                                  int32_t *cu_out, int32_t *status, int64_t n_out,
                                  const avtp_tensor *tensors, int n_tensors);
+// The budget rule run inside the selection blocks (each block for its
+// image's sequence), then the selection (and the compaction); budget[] is
+// written too.  Needs keep totals the per-image bounds can meet.
+hipError_t launch_budget_select(hipStream_t stream, const DevLayout &L, const float *img_sum,
+                                int mode, float alpha, int lo_permille, int hi_permille,
+                                int floor_abs, const float *scores, int32_t *budget,
+                                int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out,
+                                int32_t *status);
+hipError_t launch_budget_select_compact(hipStream_t stream, const DevLayout &L,
+                                        const float *img_sum, int mode, float alpha,
+                                        int lo_permille, int hi_permille, int floor_abs,
+                                        const float *scores, int32_t *budget, int32_t *keep_idx,
+                                        int64_t keep_capacity, int32_t *cu_out, int32_t *status,
+                                        int64_t n_out, const avtp_tensor *tensors, int n_tensors);
 
 // Layout of the kept tokens for the next pruning layer.
 hipError_t launch_pruned_layout(hipStream_t stream, const DevLayout &L, const int32_t *keep_idx,

@@ -2,302 +2,31 @@
 // clamp of the appendix on alpha).  One block per sequence, one thread per
 // image.
 //
-// The only floating-point step is the integer weight of every image,
-//   W_i = max(1, rint((w_i / w_max) * 2^28))
-// (w_max the largest weight of the sequence: only the ratios of the weights
-// enter the water-filling), evaluated in IEEE float64 with no contraction,
-// in a fixed operation order (documented in include/avtp.h).  Everything
-// after it is exact integer arithmetic:
-//   * the real quota q_i = clamp(lam W_i, lo_i, hi_i) with sum q_i = K lies on
-//     the segment between two consecutive breakpoints lo_i/W_i, hi_i/W_i of
-//     f(lam) = sum_i clamp(lam W_i, lo_i, hi_i); every thread evaluates f at
-//     its breakpoints by cross-multiplication (u64), block reductions pick the
-//     last breakpoint with f < K and the first with f >= K;
-//   * on that segment lam = P/Q with P = K - (pinned bounds) and Q = (free
-//     weights), so q_i = P W_i / Q for free images;
-//   * largest remainder: floor(q_i), then +1 for the K - sum floor images with
-//     the largest remainders (P W_i mod Q), lowest image index first.
-// Limits (checked on the host): n_i <= 2^20 and <= 256 images per sequence;
-// with W_i <= 2^28 every product is below 2^48 and every sum below 2^56.
+// The rule itself is in budget_rule.h (shared with the selection kernels
+// that compute their sequence's budgets in-block).
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
 
 #include "avtp_internal.h"
+#include "budget_rule.h"
 
 namespace avtp {
 namespace {
 
-constexpr int kMaxImg = AVTP_MAX_IMAGES_PER_SEQ;
-constexpr int kWeightBits = 28;
-
-// a/b < c/d for positive denominators (numerators <= 2^20, denominators <= 2^28)
-__device__ inline bool frac_lt(uint64_t a, uint64_t b, uint64_t c, uint64_t d) {
-  return a * d < c * b;
-}
-
-__device__ double image_weight(int n, long long M, float s32, double S, bool good, int mode,
-                               double alpha, int K) {
-#pragma clang fp contract(off)
-  if (n == 0) return 0.0;
-  const double u = (double)n / (double)M;
-  const double s = (double)s32;
-  double w;
-  if (!good || !isfinite(s)) {
-    w = u;
-  } else if (mode == AVTP_BUDGET_PROPORTIONAL) {
-    const double t1 = (1.0 - alpha) * u;
-    const double t2 = alpha * (s / S);
-    w = t1 + t2;
-  } else if (K > 0) {
-    const double t = u * S;
-    const double d = (s - t) / (double)K;
-    w = u + alpha * d;
-  } else {
-    w = u;
-  }
-  if (!(w > 0.0)) w = 0.0;
-  return w;
-}
-
-// One thread per image: blocks of 256 threads, or a single wave of 64 when
-// no sequence has more than 16 images (then every block-wide reduction is a
-// wave butterfly, with no LDS round trip or barrier; with more images the
-// four waves' share of the breakpoint sums pays more).
-constexpr int kThreads = 256;
-static_assert(kMaxImg <= kThreads, "one thread per image");
-
-// Block-wide sums: wave butterflies, then the four wave partials in LDS.
-template <int NTH, typename T>
-__device__ inline T block_sum(T v, T *sh) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-  if (NTH == 64) return v;
-  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
-  __syncthreads();
-  const T r = sh[0] + sh[1] + sh[2] + sh[3];
-  __syncthreads();  // sh may be reused right away
-  return r;
-}
-
-// Block-wide extreme of fractions num/den (den > 0) among the threads with
-// ok set: the smallest (MIN) or the largest.  Returns ok = false if none.
-template <bool MIN, int NTH>
-__device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, uint64_t *shn,
-                                      uint64_t *shd, int *sho) {
-  auto better = [](uint64_t an, uint64_t ad, uint64_t bn, uint64_t bd) {
-    return MIN ? frac_lt(an, ad, bn, bd) : frac_lt(bn, bd, an, ad);
-  };
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const uint64_t on = __shfl_xor(num, off), od = __shfl_xor(den, off);
-    const bool oo = __shfl_xor((int)ok, off) != 0;
-    if (oo && (!ok || better(on, od, num, den))) {
-      num = on;
-      den = od;
-      ok = true;
-    }
-  }
-  if (NTH == 64) return;
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    shn[w] = num;
-    shd[w] = den;
-    sho[w] = ok;
-  }
-  __syncthreads();
-  ok = false;
-  for (int t = 0; t < 4; ++t) {
-    if (sho[t] && (!ok || better(shn[t], shd[t], num, den))) {
-      num = shn[t];
-      den = shd[t];
-      ok = true;
-    }
-  }
-  __syncthreads();
-}
-
 template <int NTH>
 __global__ __launch_bounds__(NTH) void budget_kernel(const float *__restrict__ img_sum,
-                                                          const int32_t *__restrict__ img_len,
-                                                          const int32_t *__restrict__ cu_img,
-                                                          const int32_t *__restrict__ keep_total,
-                                                          int mode, float alpha, int lo_pm, int hi_pm,
-                                                          int floor_abs, int32_t *__restrict__ budget,
-                                                          int32_t *__restrict__ status) {
-  __shared__ uint64_t W[kMaxImg], rem[kMaxImg];
-  __shared__ uint64_t fpart[NTH];  // partial f of a breakpoint, one per thread
-  __shared__ int32_t lo[kMaxImg], hi[kMaxImg];
-  __shared__ float sv[kMaxImg];
-  __shared__ long long red_i[4];
-  __shared__ uint64_t red_u[4], ext_n[4], ext_d[4];
-  __shared__ int ext_o[4];
-  __shared__ double sh_S, red_d[4];
-
-  const int b = blockIdx.x, tid = threadIdx.x;
-  const int i0 = cu_img[b], m = cu_img[b + 1] - i0;
-  const long long K = keep_total[b];
-  if (m <= 0) return;
-  const bool mine = tid < m;  // this thread's image is tid
-
-  long long n = 0, l = 0, h = 0;
-  float s32 = 0.f;
-  if (mine) {
-    n = img_len[i0 + tid];
-    s32 = img_sum[i0 + tid];
-    l = (lo_pm * n + 999) / 1000;
-    if (l < floor_abs) l = floor_abs;
-    if (l > n) l = n;
-    h = (hi_pm * n) / 1000;
-    if (h < l) h = l;
-    lo[tid] = (int32_t)l;
-    hi[tid] = (int32_t)h;
-    sv[tid] = s32;
-  }
-  const long long M = block_sum<NTH>(n, red_i);
-  const long long slo = block_sum<NTH>(l, red_i);
-  const long long shi = block_sum<NTH>(h, red_i);
-  if (NTH == 64) __syncthreads();  // sv is read by thread 0 below
-  if (tid == 0) {  // the image sum, in image order (it fixes the weights)
-    double S = 0.0;
-    for (int i = 0; i < m; ++i) S = S + (double)sv[i];
-    sh_S = S;
-  }
-  __syncthreads();
-  const double S = sh_S;
-  const bool good = isfinite(S) && S > 0.0;
-  double w = 0.0;
-  if (mine) w = image_weight((int)n, M, s32, S, good, mode, (double)alpha, (int)K);
-  // the largest weight (weights are >= 0; images without tokens have none)
-  double wmax = w;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) wmax = fmax(wmax, __shfl_xor(wmax, off));
-  if (NTH > 64) {
-    if ((tid & 63) == 0) red_d[tid >> 6] = wmax;
-    __syncthreads();
-    wmax = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
-  }
-  uint64_t Wi = 0;
-  if (mine) {
-    if (n > 0) {
-      if (wmax > 0.0) {
-#pragma clang fp contract(off)
-        const double r = w / wmax;
-        Wi = (uint64_t)rint(r * (double)(1ll << kWeightBits));
-      }
-      if (Wi < 1) Wi = 1;
-    }
-    W[tid] = Wi;
-  }
-  if (K < slo || K > shi) {  // the host checks this too; keep outputs defined anyway
-    if (mine) budget[i0 + tid] = (int32_t)l;
-    if (tid == 0 && status) atomicOr(status + b, AVTP_FLAG_INFEASIBLE);
-    return;
-  }
-  __syncthreads();
-
-  // Breakpoints k < m: lo_k / W_k, k >= m: hi_(k-m) / W_(k-m) (zero-length
-  // images have none).  f is evaluated at every breakpoint; each thread keeps
-  // the smallest breakpoint with f >= K (next) and the largest with f < K
-  // (prev).  With few breakpoints, np threads share one breakpoint's sum
-  // over the images (np parts, combined in LDS; integer sums, so exact).
-  bool hn = false, hp = false;
-  uint64_t bn = 0, bd = 1, pn = 0, pd = 1;
-  auto partial_f = [&](uint64_t num, uint64_t den, int j0, int j1) __attribute__((always_inline)) {
-    uint64_t f = 0;  // f(num/den) * den over images j0 .. j1-1
-#pragma unroll 4
-    for (int j = j0; j < j1; ++j) {
-      const uint64_t wj = W[j];
-      if (wj == 0) continue;
-      uint64_t v = num * wj;
-      const uint64_t lj = (uint64_t)lo[j] * den, hj = (uint64_t)hi[j] * den;
-      v = v < lj ? lj : (v > hj ? hj : v);
-      f += v;
-    }
-    return f;
-  };
-  auto keep_ext = [&](uint64_t f, uint64_t num, uint64_t den) __attribute__((always_inline)) {
-    // value selects (not stores through a chosen reference), so that the six
-    // values stay in registers
-    const bool ge = f >= (uint64_t)K * den;
-    const bool tn = ge && (!hn || frac_lt(num, den, bn, bd));
-    const bool tp = !ge && (!hp || frac_lt(pn, pd, num, den));
-    bn = tn ? num : bn;
-    bd = tn ? den : bd;
-    hn = hn || tn;
-    pn = tp ? num : pn;
-    pd = tp ? den : pd;
-    hp = hp || tp;
-  };
-  const int nbp = 2 * m;
-  const int np = nbp <= NTH / 4 ? 4 : (nbp <= NTH / 2 ? 2 : 1);  // parts; block-uniform
-  if (np > 1) {
-    const int KB = NTH / np;  // >= nbp
-    const int k = tid % KB, part = tid / KB;
-    const int per = (m + np - 1) / np, j0 = min(m, part * per), j1 = min(m, j0 + per);
-    bool ok = false;
-    uint64_t num = 0, den = 1, f = 0;
-    if (k < nbp) {
-      const int i = k < m ? k : k - m;
-      if (W[i] != 0) {
-        ok = true;
-        num = (uint64_t)(k < m ? lo[i] : hi[i]);
-        den = W[i];
-        f = partial_f(num, den, j0, j1);
-      }
-    }
-    fpart[tid] = f;
-    __syncthreads();
-    if (part == 0 && ok) {
-      for (int q = 1; q < np; ++q) f += fpart[q * KB + k];
-      keep_ext(f, num, den);
-    }
-  } else {
-    for (int k = tid; k < nbp; k += NTH) {
-      const int i = k < m ? k : k - m;
-      if (W[i] == 0) continue;
-      const uint64_t num = (uint64_t)(k < m ? lo[i] : hi[i]), den = W[i];
-      keep_ext(partial_f(num, den, 0, m), num, den);
-    }
-  }
-  block_frac_ext<true, NTH>(bn, bd, hn, ext_n, ext_d, ext_o);
-  block_frac_ext<false, NTH>(pn, pd, hp, ext_n, ext_d, ext_o);
-
-  // classify the images on the segment (prev, next]: pinned at lo, at hi, or free
-  int32_t kk = 0;
-  uint64_t pinned = 0, freeW = 0;
-  bool fr = false;
-  if (mine && Wi != 0) {
-    const bool low = hn && !frac_lt((uint64_t)l, Wi, bn, bd);   // lo/W >= next
-    const bool high = hp && !frac_lt(pn, pd, (uint64_t)h, Wi);  // hi/W <= prev
-    if (low || !hn) {
-      kk = (int32_t)l;
-      pinned = (uint64_t)l;
-    } else if (high) {
-      kk = (int32_t)h;
-      pinned = (uint64_t)h;
-    } else {
-      fr = true;
-      freeW = Wi;
-    }
-  }
-  const uint64_t P = (uint64_t)K - block_sum<NTH>(pinned, red_u);
-  const uint64_t Q = block_sum<NTH>(freeW, red_u);
-  uint64_t ri = 0;
-  if (fr) {
-    const uint64_t num = P * Wi;
-    kk = (int32_t)(num / Q);
-    ri = num % Q;
-  }
-  if (mine) rem[tid] = ri;
-  if (NTH == 64) __syncthreads();  // rem is read by every lane below
-  const long long D = K - block_sum<NTH>((long long)kk, red_i);  // the units left to hand out
-  // largest remainders first, lowest image index among equal ones
-  if (mine) {
-    long long rank = 0;
-    for (int j = 0; j < m; ++j) rank += (rem[j] > ri) || (rem[j] == ri && j < tid);
-    budget[i0 + tid] = kk + (rank < D ? 1 : 0);
-  }
+                                                     const int32_t *__restrict__ img_len,
+                                                     const int32_t *__restrict__ cu_img,
+                                                     const int32_t *__restrict__ keep_total,
+                                                     int mode, float alpha, int lo_pm, int hi_pm,
+                                                     int floor_abs, int32_t *__restrict__ budget,
+                                                     int32_t *__restrict__ status) {
+  const int b = blockIdx.x;
+  int32_t *out = budget + cu_img[b];
+  budget_rule::seq_budget<NTH>(b, img_sum, img_len, cu_img, keep_total, mode, alpha, lo_pm, hi_pm,
+                               floor_abs, status,
+                               [&](int t, int32_t v) __attribute__((always_inline)) { out[t] = v; });
 }
 
 }  // namespace
@@ -310,9 +39,10 @@ hipError_t launch_budget(hipStream_t st, const DevLayout &L, const float *img_su
                        L.keep_total, mode, alpha, lo_permille, hi_permille, floor_abs, budget,
                        status);
   else
-    hipLaunchKernelGGL(budget_kernel<kThreads>, dim3(L.B), dim3(kThreads), 0, st, img_sum,
-                       L.img_len, L.cu_img, L.keep_total, mode, alpha, lo_permille, hi_permille,
-                       floor_abs, budget, status);
+    hipLaunchKernelGGL(budget_kernel<budget_rule::kThreads>, dim3(L.B),
+                       dim3(budget_rule::kThreads), 0, st, img_sum, L.img_len, L.cu_img,
+                       L.keep_total, mode, alpha, lo_permille, hi_permille, floor_abs, budget,
+                       status);
   return hipGetLastError();
 }
 

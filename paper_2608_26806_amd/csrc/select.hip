@@ -16,6 +16,7 @@
 #include <stdint.h>
 
 #include "avtp_internal.h"
+#include "budget_rule.h"
 #include "row_copy.h"
 
 namespace avtp {
@@ -32,9 +33,76 @@ __device__ inline uint32_t order_key(float s) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+__device__ inline int clamp_budget(int k, int n) { return k < 0 ? 0 : (k > n ? n : k); }
 __device__ inline int eff_budget(const int32_t *budget, const int32_t *img_len, int i) {
-  const int k = budget[i], n = img_len[i];
-  return k < 0 ? 0 : (k > n ? n : k);
+  return clamp_budget(budget[i], img_len[i]);
+}
+
+// Where a selection block takes the budgets from.  part(i): this thread's
+// share of the budgets of every image before i (the block sums the shares);
+// k(i): image i's budget, clamped to [0, len].
+struct BudGlobal {  // written by the budget kernel
+  const int32_t *budget, *img_len;
+  __device__ long long part(int i) const {
+    long long p = 0;
+    for (int j = threadIdx.x; j < i; j += kThreads) p += eff_budget(budget, img_len, j);
+    return p;
+  }
+  __device__ int k(int i) const { return eff_budget(budget, img_len, i); }
+};
+struct BudInBlock {  // computed by the block for its own sequence b (in LDS)
+  const int32_t *bud;  // budgets of b's images, index j - i0
+  const int32_t *img_len, *keep_total;
+  int b, i0;
+  // every earlier sequence keeps exactly its keep_total (the host rejects
+  // totals its bounds cannot meet, and the rule hands out exactly K)
+  __device__ long long part(int i) const {
+    long long p = 0;
+    for (int c = threadIdx.x; c < b; c += kThreads) p += keep_total[c];
+    for (int j = i0 + threadIdx.x; j < i; j += kThreads) p += clamp_budget(bud[j - i0], img_len[j]);
+    return p;
+  }
+  __device__ int k(int i) const { return clamp_budget(bud[i - i0], img_len[i]); }
+};
+
+// The budget rule's inputs, for the kernels that run it in-block.
+struct RuleArgs {
+  const float *img_sum;
+  const int32_t *keep_total;
+  int mode;
+  float alpha;
+  int lo_pm, hi_pm, floor_abs;
+  int32_t *budget;  // every image's budget is also written here (by one block)
+};
+
+// The sequence of image i (block-uniform; i < n_img).
+__device__ inline int seq_of_image(const int32_t *cu_img, int B, int i) {
+  __shared__ int sh;
+  for (int c = threadIdx.x; c < B; c += kThreads)
+    if (cu_img[c] <= i && i < cu_img[c + 1]) sh = c;
+  __syncthreads();
+  const int b = sh;
+  __syncthreads();  // (sh may be written again by the next call)
+  return b;
+}
+
+// Runs the budget rule for image i's sequence into LDS and returns the
+// matching policy.  The block with write set stores budget[i] (one block
+// per image does), and the one of the sequence's first image the
+// infeasibility flag.
+__device__ __attribute__((always_inline)) inline BudInBlock budgets_in_block(
+    const RuleArgs &R, const int32_t *img_len, const int32_t *cu_img, int B, int i, bool write,
+    int32_t *status) {
+  __shared__ int32_t bud[AVTP_MAX_IMAGES_PER_SEQ];
+  const int b = seq_of_image(cu_img, B, i);
+  const int i0 = cu_img[b];
+  budget_rule::seq_budget<kThreads>(b, R.img_sum, img_len, cu_img, R.keep_total, R.mode, R.alpha,
+                                    R.lo_pm, R.hi_pm, R.floor_abs,
+                                    write && i == i0 ? status : nullptr,
+                                    [&](int t, int32_t v) __attribute__((always_inline)) { bud[t] = v; });
+  __syncthreads();
+  if (write && threadIdx.x == 0) R.budget[i] = bud[i - i0];
+  return BudInBlock{bud, img_len, R.keep_total, b, i0};
 }
 
 // exclusive block scan of a 0/1 flag (256 threads, 4 waves); returns the
@@ -126,8 +194,9 @@ struct SelArgs {
 
 // The kept tokens of image i (and the text rows around it), reported as
 // put(output index, token index, sequence) in no particular order.
-template <typename Put>
-__device__ __attribute__((always_inline)) inline void select_image(const SelArgs &A, int i, Put put) {
+template <typename Put, typename Bud>
+__device__ __attribute__((always_inline)) inline void select_image(const SelArgs &A, int i, Put put,
+                                                                   const Bud &bud) {
   __shared__ uint32_t hist[2][256];  // double-buffered across the radix passes
   __shared__ uint32_t keys[kLdsKeys];
   __shared__ int wsum[4];
@@ -136,7 +205,6 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   __shared__ int sh_krem[4], sh_b;
   const int tid = threadIdx.x;
   const float *__restrict__ scores = A.scores;
-  const int32_t *__restrict__ budget = A.budget;
   const int32_t *__restrict__ img_start = A.img_start;
   const int32_t *__restrict__ img_len = A.img_len;
   const int32_t *__restrict__ cu_img = A.cu_img;
@@ -155,9 +223,8 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   for (int c = tid; c < B; c += kThreads)  // the sequence holding image i
     if (cu_img[c] <= i && i < cu_img[c + 1]) sh_b = c;
   const int st = img_start[i], n = img_len[i];
-  const int k = eff_budget(budget, img_len, i);
-  long long part = 0;  // budgets of the images before i
-  for (int j = tid; j < i; j += kThreads) part += eff_budget(budget, img_len, j);
+  const int k = bud.k(i);
+  const long long part = bud.part(i);  // (this thread's share of) the budgets of the images before i
   // the image's order keys into LDS now: their loads overlap the prefix and
   // text-row reductions below (whose barriers also order them before the
   // radix passes)
@@ -273,13 +340,24 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   }
 }
 
-__global__ __launch_bounds__(kThreads) void select_kernel(SelArgs A, int32_t *__restrict__ keep_idx,
+// INB: the block first runs the budget rule for its image's sequence
+// (RuleArgs) instead of reading the budget kernel's output.
+template <bool INB>
+__global__ __launch_bounds__(kThreads) void select_kernel(SelArgs A, RuleArgs R,
+                                                         int32_t *__restrict__ keep_idx,
                                                          long long cap, int32_t *__restrict__ status) {
-  select_image(A, A.n_img > 0 ? (int)blockIdx.x : 0,
-               [&](long long o, int32_t v, int seq) __attribute__((always_inline)) {
-                 if (o < cap) keep_idx[o] = v;
-                 else if (status) atomicOr(status + seq, AVTP_FLAG_OUT_CAPACITY);
-               });
+  const int i = A.n_img > 0 ? (int)blockIdx.x : 0;
+  auto put = [&](long long o, int32_t v, int seq) __attribute__((always_inline)) {
+    if (o < cap) keep_idx[o] = v;
+    else if (status) atomicOr(status + seq, AVTP_FLAG_OUT_CAPACITY);
+  };
+  if constexpr (INB) {  // (without images select_image reads no budget)
+    select_image(A, i, put,
+                 A.n_img > 0 ? budgets_in_block(R, A.img_len, A.cu_img, A.B, i, true, status)
+                             : BudInBlock{});
+  } else {
+    select_image(A, i, put, BudGlobal{A.budget, A.img_len});
+  }
 }
 
 // Fused selection and compaction: S blocks per image (slices).  Every slice
@@ -316,7 +394,8 @@ __device__ inline void copy_listed(const CTensor &T, const int *lo, const int *l
                          });
 }
 
-__global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a) {
+template <bool INB>
+__global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a, RuleArgs R) {
   __shared__ int list_o[kListCap], list_j[kListCap];
   __shared__ int list_n;
   const int S = a.S;
@@ -325,7 +404,7 @@ __global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a) {
   __syncthreads();
   SelArgs A = a.sel;
   if (sl != 0) A.cu_out = nullptr;
-  select_image(A, img, [&](long long o, int32_t v, int seq) __attribute__((always_inline)) {
+  auto put = [&](long long o, int32_t v, int seq) __attribute__((always_inline)) {
     if ((int)(o % S) != sl) return;
     if (o >= a.cap) {
       if (a.status) atomicOr(a.status + seq, AVTP_FLAG_OUT_CAPACITY);
@@ -340,7 +419,14 @@ __global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a) {
     } else if (a.status) {  // (the host sizes S so that this does not happen)
       atomicOr(a.status + seq, AVTP_FLAG_OUT_CAPACITY);
     }
-  });
+  };
+  if constexpr (INB) {
+    select_image(A, img, put,
+                 A.n_img > 0 ? budgets_in_block(R, A.img_len, A.cu_img, A.B, img, sl == 0, a.status)
+                             : BudInBlock{});
+  } else {
+    select_image(A, img, put, BudGlobal{A.budget, A.img_len});
+  }
   __syncthreads();
   const int n = min(list_n, kListCap);
   for (int ti = 0; ti < a.n_t; ++ti) {
@@ -355,12 +441,24 @@ __global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a) {
   }
 }
 
-}  // namespace
+// Blocks per image of the one-launch selection + compaction: about 1024
+// blocks in all, and few enough rows per slice for its list (an image block
+// writes at most the image's tokens plus every text row; each contiguous run
+// adds at most one to a share).
+static int compact_slices(const DevLayout &L) {
+  const long long bound = (long long)L.max_img_len + L.T_tot + 64;
+  const int images = L.n_img > 0 ? L.n_img : 1;
+  long long S = (1024 + images - 1) / images;
+  if (S > 64) S = 64;
+  const long long need = (bound + (kListCap - 64) - 1) / (kListCap - 64);
+  if (S < need) S = need;
+  if (S < 1) S = 1;
+  return (int)S;
+}
 
-hipError_t launch_select_compact(hipStream_t st, const DevLayout &L, const float *scores,
-                                 const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
-                                 int32_t *cu_out, int32_t *status, int64_t n_out,
-                                 const avtp_tensor *tensors, int n_tensors) {
+static SCArgs sc_args(const DevLayout &L, const float *scores, const int32_t *budget,
+                      int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out, int32_t *status,
+                      int64_t n_out, const avtp_tensor *tensors, int n_tensors) {
   SCArgs a;
   a.sel = SelArgs{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
                   L.B, L.n_img, L.T_tot, cu_out};
@@ -370,18 +468,26 @@ hipError_t launch_select_compact(hipStream_t st, const DevLayout &L, const float
   a.status = status;
   a.n_t = n_tensors;
   for (int i = 0; i < n_tensors; ++i) describe_tensor(tensors[i], kThreads, a.t[i]);
-  // slices per image: about 1024 blocks in all, and few enough rows per
-  // slice for its list (an image block writes at most the image's tokens
-  // plus every text row; each contiguous run adds at most one to a share)
-  const long long bound = (long long)L.max_img_len + L.T_tot + 64;
+  a.S = compact_slices(L);
+  return a;
+}
+
+static RuleArgs rule_args(const DevLayout &L, const float *img_sum, int mode, float alpha,
+                          int lo_permille, int hi_permille, int floor_abs, int32_t *budget) {
+  return RuleArgs{img_sum, L.keep_total, mode, alpha, lo_permille, hi_permille, floor_abs, budget};
+}
+
+}  // namespace
+
+hipError_t launch_select_compact(hipStream_t st, const DevLayout &L, const float *scores,
+                                 const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
+                                 int32_t *cu_out, int32_t *status, int64_t n_out,
+                                 const avtp_tensor *tensors, int n_tensors) {
+  const SCArgs a = sc_args(L, scores, budget, keep_idx, keep_capacity, cu_out, status, n_out,
+                           tensors, n_tensors);
   const int images = L.n_img > 0 ? L.n_img : 1;
-  long long S = (1024 + images - 1) / images;
-  if (S > 64) S = 64;
-  const long long need = (bound + (kListCap - 64) - 1) / (kListCap - 64);
-  if (S < need) S = need;
-  if (S < 1) S = 1;
-  a.S = (int)S;
-  hipLaunchKernelGGL(select_compact_kernel, dim3((unsigned)(images * S)), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL(select_compact_kernel<false>, dim3((unsigned)(images * a.S)), dim3(kThreads),
+                     0, st, a, RuleArgs{});
   return hipGetLastError();
 }
 
@@ -391,8 +497,36 @@ hipError_t launch_select(hipStream_t st, const DevLayout &L, const float *scores
   const int grid = L.n_img > 0 ? L.n_img : 1;
   const SelArgs A{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
                   L.B, L.n_img, L.T_tot, cu_out};
-  hipLaunchKernelGGL(select_kernel, dim3(grid), dim3(kThreads), 0, st, A, keep_idx,
-                     (long long)keep_capacity, status);
+  hipLaunchKernelGGL(select_kernel<false>, dim3(grid), dim3(kThreads), 0, st, A, RuleArgs{},
+                     keep_idx, (long long)keep_capacity, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_budget_select(hipStream_t st, const DevLayout &L, const float *img_sum, int mode,
+                                float alpha, int lo_permille, int hi_permille, int floor_abs,
+                                const float *scores, int32_t *budget, int32_t *keep_idx,
+                                int64_t keep_capacity, int32_t *cu_out, int32_t *status) {
+  const int grid = L.n_img > 0 ? L.n_img : 1;
+  const SelArgs A{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
+                  L.B, L.n_img, L.T_tot, cu_out};
+  hipLaunchKernelGGL(select_kernel<true>, dim3(grid), dim3(kThreads), 0, st, A,
+                     rule_args(L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget),
+                     keep_idx, (long long)keep_capacity, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_budget_select_compact(hipStream_t st, const DevLayout &L, const float *img_sum,
+                                        int mode, float alpha, int lo_permille, int hi_permille,
+                                        int floor_abs, const float *scores, int32_t *budget,
+                                        int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out,
+                                        int32_t *status, int64_t n_out, const avtp_tensor *tensors,
+                                        int n_tensors) {
+  const SCArgs a = sc_args(L, scores, budget, keep_idx, keep_capacity, cu_out, status, n_out,
+                           tensors, n_tensors);
+  const int images = L.n_img > 0 ? L.n_img : 1;
+  hipLaunchKernelGGL(select_compact_kernel<true>, dim3((unsigned)(images * a.S)), dim3(kThreads),
+                     0, st, a,
+                     rule_args(L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget));
   return hipGetLastError();
 }
 

@@ -65,3 +65,37 @@ def kept_sets_match(layout, keep_gpu, keep_ref, scores_ref, budget_ref, tol):
         assert abs(scores_ref[j] - theta) <= tol * abs(theta), \
             f"token {j} (score {scores_ref[j]}) is not near the threshold {theta} of image {i}"
     return len(diff)
+
+
+def budget_cases():
+    """(image lengths, image sums, alpha, floor_abs, mode) of one sequence each:
+    1-32 images with empty images, zero sums and both modes, then sequences of
+    33 to 256 images."""
+    from oracle import avtp_oracle as O
+
+    rng = np.random.default_rng(77)
+    cases = []
+    for t in range(40):
+        m = int(rng.integers(1, 33))
+        n = [int(x) for x in rng.integers(1, 1600, size=m)]
+        if t % 7 == 0:
+            n[0] = 0 if m > 1 else n[0]                 # an empty image
+        alpha = [0.0, 1.0, 2.0, 5.0][t % 4]
+        floor_abs = [0, 16, 3][t % 3]
+        mode = O.BUDGET_RAW if t % 5 == 4 else O.BUDGET_PROPORTIONAL
+        S = (rng.lognormal(0.0, 1.0 + (t % 3), size=m) * np.array(n) / 100).astype(np.float32)
+        if t % 11 == 3:
+            S[:] = 0.0                                  # no importance at all
+        if t % 13 == 5:
+            S[int(rng.integers(0, m))] = 0.0
+        cases.append((n, S, alpha, floor_abs, mode))
+    # more images per sequence than 32: the kernel splits each breakpoint's
+    # sum over 4 threads up to 32 images, over 2 up to 64, and not above
+    for t, m in enumerate([33, 48, 64, 65, 100, 128, 129, 200, 256]):
+        n = [int(x) for x in rng.integers(1, 400, size=m)]
+        alpha = [1.0, 2.0, 0.0][t % 3]
+        floor_abs = [0, 16][t % 2]
+        mode = O.BUDGET_RAW if t % 4 == 3 else O.BUDGET_PROPORTIONAL
+        S = (rng.lognormal(0.0, 2.0, size=m) * np.array(n) / 100).astype(np.float32)
+        cases.append((n, S, alpha, floor_abs, mode))
+    return cases

@@ -177,6 +177,40 @@ def test_select_compact_arguments_rejected_on_host():
     assert lib.avtp_select_compact(None, dl.ref(), p, p, p, 100, p, None, t, 1) == A.ERR_INVALID_ARG  # null src
 
 
+def test_budget_select_compact_arguments_rejected_on_host():
+    """The one-call budget + selection + compaction checks the arguments of
+    all three calls, feasibility included, before any launch."""
+    lib = A.lib()
+    buf = torch.zeros(256, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    t = (A._Tensor * 1)()
+    f = lib.avtp_budget_select_compact
+    lay = build_layout([[20, 20]], 2, 1, 50)
+    dl = _dl(lay)
+    ok = (p, 0, 1.0, 50, 950, 0, p, p, p, 100, p, None, t, 0)   # img_sum .. n_tensors
+    assert f(None, None, *ok) == A.ERR_INVALID_ARG
+    assert f(None, _dl(lay, keep_total=np.array([39])).ref(), *ok) == A.ERR_INFEASIBLE  # sum hi 38
+    assert f(None, _dl(lay, keep_total=np.array([10])).ref(),
+             p, 0, 1.0, 50, 950, 8, *ok[6:]) == A.ERR_INFEASIBLE                      # floors 16
+    bad = [(2, -1.0), (2, 33.0), (1, 5), (3, 960)]                 # alpha, mode, lo > hi
+    for pos, val in bad:
+        args = list(ok)
+        args[pos] = val
+        assert f(None, dl.ref(), *args) == A.ERR_INVALID_ARG, (pos, val)
+    for pos in (0, 6, 7, 10):                                      # img_sum, scores, budget, cu_out
+        args = list(ok)
+        args[pos] = None
+        assert f(None, dl.ref(), *args) == A.ERR_INVALID_ARG, pos
+    args = list(ok)
+    args[9] = dl.N_out - 1                                         # keep capacity
+    assert f(None, dl.ref(), *args) == A.ERR_INVALID_ARG
+    args = list(ok)
+    args[13] = 9
+    assert f(None, dl.ref(), *args) == A.ERR_UNSUPPORTED          # too many tensors
+    args[13] = 1
+    assert f(None, dl.ref(), *args) == A.ERR_INVALID_ARG          # null src
+
+
 def test_noalloc_rejects_oversize_and_bad_args_on_the_host():
     """avtp_score_noalloc checks every argument, and that the layout fits its
     scratch, before any HIP call (so this runs without a GPU)."""

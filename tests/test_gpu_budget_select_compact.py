@@ -1,0 +1,143 @@
+"""GPU parity of avtp_budget_select_compact (budgets, selection and compaction
+in one call) against the oracle and against avtp_budget, avtp_select and
+avtp_compact called one after the other: budgets, kept indices, cu_out and
+every compacted tensor bit-exact.
+
+While no sequence has more than 64 images every selection block runs the
+budget rule for its own sequence; above that the budget kernel runs first.
+Both paths are taken here, each with several sequences per call (the kept
+rows of a sequence start after every earlier sequence's keep total)."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import budget_cases, need_gpu, say, to_dev, to_host_bits
+from oracle import avtp_oracle as O
+from paper_2608_26806_amd import avtp as A
+from paper_2608_26806_amd.workloads import build_layout, make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    need_gpu()
+    A.lib()
+
+
+def _keeps(seqs, fa, rng):
+    out = []
+    for n in seqs:
+        lo = sum(O.budget_bounds(x, 50, 950, fa)[0] for x in n)
+        hi = sum(O.budget_bounds(x, 50, 950, fa)[1] for x in n)
+        out.append(int(rng.integers(lo, hi + 1)))
+    return out
+
+
+def _run_and_check(seqs, sums, alpha, fa, mode, rng, pre=2, tail=3, tag=""):
+    """One call over the sequences seqs (image lengths) with image sums sums;
+    every output against the oracle."""
+    lay = build_layout(seqs, pre, tail, 0)
+    lay.keep_total[:] = _keeps(seqs, fa, rng)
+    dl = A.DeviceLayout(lay)
+    S = np.concatenate([np.asarray(x, np.float32) for x in sums]) if lay.n_img else \
+        np.zeros(1, np.float32)
+    s = rng.standard_normal(lay.N_tok).astype(np.float32)
+    say(f"[budget_select_compact] {tag} B={lay.B} images={lay.n_img} "
+        f"max/seq={max((len(n) for n in seqs), default=0)} alpha={alpha} floor={fa} mode={mode}")
+    hid = torch.randn(lay.N_tok, 40, device="cuda").to(torch.bfloat16)
+    pos = torch.randint(0, 1 << 40, (3, lay.N_tok), dtype=torch.int64, device="cuda")
+    out_h = torch.empty((dl.N_out, 40), dtype=torch.bfloat16, device="cuda")
+    out_p = torch.empty((3, dl.N_out), dtype=torch.int64, device="cuda")
+    status = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+    bud, keep, cu = A.budget_select_compact(
+        dl, torch.from_numpy(S).cuda(), torch.from_numpy(s).cuda(),
+        [(hid, out_h, 0), (pos, out_p, 1)], alpha, 50, 950, fa, mode, status=status)
+    torch.cuda.synchronize()
+    bud_o = O.budget(lay, S[:lay.n_img], alpha, 50, 950, fa, mode)
+    assert np.array_equal(bud.cpu().numpy(), bud_o)
+    keep_o, cu_o = O.select(lay, s, bud_o)
+    assert keep.cpu().numpy().tolist() == keep_o.tolist()
+    assert cu.cpu().numpy().tolist() == cu_o.tolist()
+    idx = torch.from_numpy(keep_o.astype(np.int64)).cuda()
+    assert torch.equal(out_h, hid[idx])
+    assert torch.equal(out_p, pos[:, idx])
+    assert not status.any()
+
+
+def test_budget_cases_grouped_in_one_call():
+    # the budget tests' sequences (1-32 images, empty images, zero sums, both
+    # modes), those with equal rule parameters batched into one call each
+    cases = budget_cases()[:40]
+    rng = np.random.default_rng(41)
+    groups = {}
+    for n, S, alpha, fa, mode in cases:
+        groups.setdefault((alpha, fa, mode), []).append((n, S))
+    assert len(groups) > 1 and max(len(g) for g in groups.values()) > 1
+    for (alpha, fa, mode), g in sorted(groups.items()):
+        _run_and_check([n for n, _ in g], [S for _, S in g], alpha, fa, mode, rng, tag="group")
+
+
+@pytest.mark.parametrize("m", [33, 64, 65, 256])
+def test_many_images_per_sequence(m):
+    # up to 64 images the selection blocks run the rule; 65 and 256 take the
+    # budget kernel first
+    rng = np.random.default_rng(m)
+    seqs = [[int(x) for x in rng.integers(1, 300, size=m)], [17, 5], []]
+    sums = [(rng.lognormal(0.0, 2.0, size=len(n)) * np.array(n, float) / 100).astype(np.float32)
+            for n in seqs]
+    _run_and_check(seqs, sums, 1.0, 8, O.BUDGET_PROPORTIONAL, rng, tag=f"m={m}")
+
+
+def test_many_sequences():
+    # more sequences than a block has threads: the keep totals of all earlier
+    # sequences are summed in strides; some sequences have no images
+    rng = np.random.default_rng(300)
+    seqs = [[int(x) for x in rng.integers(0, 60, size=int(rng.integers(0, 4)))] for _ in range(300)]
+    sums = [(rng.random(len(n)) * np.array(n, float)).astype(np.float32) for n in seqs]
+    _run_and_check(seqs, sums, 2.0, 0, O.BUDGET_RAW, rng, pre=1, tail=2, tag="300 sequences")
+
+
+def test_text_only_batch():
+    rng = np.random.default_rng(3)
+    _run_and_check([[], []], [[], []], 1.0, 0, O.BUDGET_PROPORTIONAL, rng, pre=0, tail=5,
+                   tag="text only")
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_one_call_equals_separate_calls(cfg):
+    # configs 1-2 move at most 32 MiB (one launch); 3-5 more (the selection
+    # blocks with in-block budgets, then the compaction kernel)
+    wl = make_workload(cfg, payload=True)
+    lay = wl.layout
+    dl = A.DeviceLayout(lay)
+    say(f"[budget_select_compact] config {cfg}")
+    rng = np.random.default_rng(100 + cfg)
+    s = rng.random(lay.N_tok).astype(np.float32)
+    isum = np.array([s[a:a + n].sum() for a, n in zip(lay.img_start, lay.img_len)], np.float32)
+    sd, id_ = torch.from_numpy(s).cuda(), torch.from_numpy(isum).cuda()
+    hid = to_dev(wl.hidden_states, wl.dtype)
+    pos = torch.from_numpy(wl.pos).cuda()
+    kd, vd = to_dev(wl.k, wl.dtype), to_dev(wl.v, wl.dtype)
+    srcs = [(hid, 0), (pos, 1), (kd, 0), (vd, 0)]
+    args = (wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs)
+    st_a = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+    bud_a = A.budget(dl, id_, *args, status=st_a)
+    keep_a, cu_a = A.select(dl, sd, bud_a, status=st_a)
+    outs_a = A.compact_new(dl, keep_a, srcs)
+    pairs, outs_b = [], []
+    for src, tdim in srcs:
+        shape = list(src.shape)
+        shape[tdim] = dl.N_out
+        dst = torch.empty(shape, dtype=src.dtype, device="cuda")
+        outs_b.append(dst)
+        pairs.append((src, dst, tdim))
+    st_b = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+    bud_b, keep_b, cu_b = A.budget_select_compact(dl, id_, sd, pairs, *args, status=st_b)
+    torch.cuda.synchronize()
+    assert torch.equal(bud_a, bud_b)
+    assert np.array_equal(bud_b.cpu().numpy(), O.budget(lay, isum, *args))
+    assert torch.equal(keep_a, keep_b) and torch.equal(cu_a, cu_b)
+    assert torch.equal(st_a, st_b) and not st_b.any()
+    for x, y in zip(outs_a, outs_b):
+        assert np.array_equal(to_host_bits(x), to_host_bits(y))

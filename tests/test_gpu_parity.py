@@ -15,7 +15,8 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import (TOL, assert_rel, kept_sets_match, need_gpu, say, to_dev, to_host_bits)
+from gpu_util import (TOL, assert_rel, budget_cases, kept_sets_match, need_gpu, say, to_dev,
+                      to_host_bits)
 from oracle import avtp_oracle as O
 from paper_2608_26806_amd import avtp as A
 from paper_2608_26806_amd.workloads import (Layout, build_layout, duplicate_key_rows, f32_to_bf16_bits,
@@ -185,37 +186,8 @@ def test_score_parity_launch_shapes(name):
 
 
 # ------------------------------------------------------------------ budget
-def _budget_cases():
-    rng = np.random.default_rng(77)
-    cases = []
-    for t in range(40):
-        m = int(rng.integers(1, 33))
-        n = [int(x) for x in rng.integers(1, 1600, size=m)]
-        if t % 7 == 0:
-            n[0] = 0 if m > 1 else n[0]                 # an empty image
-        alpha = [0.0, 1.0, 2.0, 5.0][t % 4]
-        floor_abs = [0, 16, 3][t % 3]
-        mode = O.BUDGET_RAW if t % 5 == 4 else O.BUDGET_PROPORTIONAL
-        S = (rng.lognormal(0.0, 1.0 + (t % 3), size=m) * np.array(n) / 100).astype(np.float32)
-        if t % 11 == 3:
-            S[:] = 0.0                                  # no importance at all
-        if t % 13 == 5:
-            S[int(rng.integers(0, m))] = 0.0
-        cases.append((n, S, alpha, floor_abs, mode))
-    # more images per sequence than 32: the kernel splits each breakpoint's
-    # sum over 4 threads up to 32 images, over 2 up to 64, and not above
-    for t, m in enumerate([33, 48, 64, 65, 100, 128, 129, 200, 256]):
-        n = [int(x) for x in rng.integers(1, 400, size=m)]
-        alpha = [1.0, 2.0, 0.0][t % 3]
-        floor_abs = [0, 16][t % 2]
-        mode = O.BUDGET_RAW if t % 4 == 3 else O.BUDGET_PROPORTIONAL
-        S = (rng.lognormal(0.0, 2.0, size=m) * np.array(n) / 100).astype(np.float32)
-        cases.append((n, S, alpha, floor_abs, mode))
-    return cases
-
-
 def test_budget_bit_exact_on_same_image_sums():
-    cases = _budget_cases()
+    cases = budget_cases()
     rng = np.random.default_rng(5)
     imgs, sums, keeps = [], [], []
     for n, S, alpha, fa, mode in cases:
