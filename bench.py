@@ -23,6 +23,7 @@ cores, and one single-thread run for configs 1-2).
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -367,10 +368,11 @@ def measure_layer(wl, dev, steps, warmup):
 
     The timed step is two calls of the C ABI: avtp_score in its plain
     two-pass form, then avtp_budget_select_compact (budgets, selection and
-    the compaction of hidden states, position ids, K and V), HIP events
-    between the calls.  The same layer as four calls (avtp_score, avtp_budget,
-    avtp_select, avtp_compact) is timed after it, events between the calls,
-    for the per-stage breakdown.  Pass 1 alone (avtp_row_lse: row statistics
+    the compaction of hidden states, position ids, K and V); the `steps`
+    steps are timed together, one HIP event pair around them.  Loops of
+    their own, events between the calls, give the split between the two
+    calls and the same layer as four calls (avtp_score, avtp_budget,
+    avtp_select, avtp_compact) for the per-stage breakdown.  Pass 1 alone (avtp_row_lse: row statistics
     + LSE combine) is timed in a loop of its own; pass 2's time is the score
     call's minus pass 1's."""
     import torch
@@ -406,20 +408,22 @@ def measure_layer(wl, dev, steps, warmup):
                           p[0].shape[0] * p[0][0, 0].numel() * p[0].element_size() for p in pairs)
 
     stream = torch.cuda.current_stream()
+    sh = ctypes.c_void_p(stream.cuda_stream)  # the stream handle, looked up once
+    tset = A.TensorSet(pairs)                 # the compaction's descriptors, built once
     score_call = lambda: A.score_attn(dl, q, k, wl.softmax_scale, scores=scores, img_sum=isum,
-                                      status=status, ws=ws)
+                                      status=status, ws=ws, stream=sh)
     bargs = (wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs)
     calls = [  # the timed step
         score_call,
-        lambda: A.budget_select_compact(dl, isum, scores, pairs, *bargs, budget_out=bud,
-                                        keep_idx=keep, cu_out=cu_out, status=status),
+        lambda: A.budget_select_compact(dl, isum, scores, tset, *bargs, budget_out=bud,
+                                        keep_idx=keep, cu_out=cu_out, status=status, stream=sh),
     ]
     names = ["score", "budget", "select", "compact"]
     calls4 = [  # the same layer as four calls
         score_call,
-        lambda: A.budget(dl, isum, *bargs, out=bud, status=status),
-        lambda: A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status),
-        lambda: A.compact(dl, keep, pairs),
+        lambda: A.budget(dl, isum, *bargs, out=bud, status=status, stream=sh),
+        lambda: A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status, stream=sh),
+        lambda: A.compact(dl, keep, tset, stream=sh),
     ]
 
     def step(cs, ev=None):
@@ -448,21 +452,33 @@ def measure_layer(wl, dev, steps, warmup):
 
     for _ in range(warmup):
         step(calls)
+    # the timed steps: one event pair around all of them (events between the
+    # calls would add their own host time to every step)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    per2, layer_ms, wall = run(calls, steps)           # the timed steps
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        step(calls)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_layer = e0.elapsed_time(e1) / steps
+    per2, _, _ = run(calls, max(steps, 10))            # score / prune split, events between
     per, layer4_ms, _ = run(calls4, max(steps, 10))    # the four-call breakdown
     st = status.cpu().numpy()
     if st.any():
         print(f"warning: device status flags {st.tolist()}", file=sys.stderr)
     reps = max(steps, 10)
-    t_p1 = _events(stream, lambda: A.row_lse(dl, q, k, wl.softmax_scale, out=lse, ws=ws), reps) * 1e-3
+    t_p1 = _events(stream, lambda: A.row_lse(dl, q, k, wl.softmax_scale, out=lse, ws=ws, stream=sh),
+                   reps) * 1e-3
     # the fused call and the two separate calls, timed the same way (events
     # around each call, or around the pair)
-    fused_us = _events(stream, lambda: A.select_compact(dl, scores, bud, pairs), reps)
+    fused_us = _events(stream, lambda: A.select_compact(dl, scores, bud, tset, stream=sh), reps)
 
     def _sep():
-        A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status)
-        A.compact(dl, keep, pairs)
+        A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status, stream=sh)
+        A.compact(dl, keep, tset, stream=sh)
 
     sep_us = _events(stream, _sep, reps)
 
@@ -470,13 +486,12 @@ def measure_layer(wl, dev, steps, warmup):
     # attention hands it over): pass 2 only, then budget, select, compact
     def _layer_lse():
         A.score_attn(dl, q, k, wl.softmax_scale, row_lse=lse, scores=scores, img_sum=isum,
-                     status=status, ws=ws)
+                     status=status, ws=ws, stream=sh)
         calls[1]()
 
     lse_layer_us = _events(stream, _layer_lse, reps)
 
     M = int(lay.img_len.sum())
-    ms_layer = float(np.median(layer_ms))
     ms = {n: float(np.mean(per[:, j])) for j, n in enumerate(names)}
     ms_score = float(np.mean(per2[:, 0]))
     ms_prune = float(np.mean(per2[:, 1]))

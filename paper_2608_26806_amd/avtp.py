@@ -118,6 +118,10 @@ def _ptr(t: Optional[torch.Tensor]):
 
 
 def _stream(stream=None):
+    """The HIP stream handle: torch's current stream by default; a torch
+    stream, or a raw handle (ctypes.c_void_p) passed through as is."""
+    if isinstance(stream, ctypes.c_void_p):
+        return stream
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
 
@@ -299,17 +303,33 @@ def tensor_desc(src: torch.Tensor, dst: torch.Tensor, token_dim: int = 0) -> _Te
     raise ValueError("token_dim must be 0 or 1")
 
 
-def compact(dl: DeviceLayout, keep_idx: torch.Tensor, pairs: Sequence, n_out: Optional[int] = None,
+class TensorSet:
+    """The descriptors of a compaction's (src, dst[, token_dim]) pairs, built
+    once; pass it wherever pairs are taken to skip rebuilding them on every
+    call (it keeps the tensors alive)."""
+
+    def __init__(self, pairs: Sequence):
+        self.pairs = list(pairs)
+        descs = [tensor_desc(p[0], p[1], p[2] if len(p) > 2 else 0) for p in self.pairs]
+        self.n = len(descs)
+        self.arr = (_Tensor * max(1, self.n))(*descs)
+
+
+def _tensor_set(pairs) -> TensorSet:
+    return pairs if isinstance(pairs, TensorSet) else TensorSet(pairs)
+
+
+def compact(dl: DeviceLayout, keep_idx: torch.Tensor, pairs, n_out: Optional[int] = None,
             stream=None) -> None:
-    """pairs: (src, dst) or (src, dst, token_dim) tuples; dst is written in place."""
-    descs = [tensor_desc(p[0], p[1], p[2] if len(p) > 2 else 0) for p in pairs]
-    arr = (_Tensor * max(1, len(descs)))(*descs)
+    """pairs: (src, dst) or (src, dst, token_dim) tuples, or a TensorSet of
+    them; dst is written in place."""
+    ts = _tensor_set(pairs)
     n = dl.N_out if n_out is None else int(n_out)
-    _check(lib().avtp_compact(_stream(stream), dl.ref(), _ptr(keep_idx), n, arr, len(descs)),
+    _check(lib().avtp_compact(_stream(stream), dl.ref(), _ptr(keep_idx), n, ts.arr, ts.n),
            "avtp_compact")
 
 
-def select_compact(dl: DeviceLayout, scores: torch.Tensor, budget_: torch.Tensor, pairs: Sequence,
+def select_compact(dl: DeviceLayout, scores: torch.Tensor, budget_: torch.Tensor, pairs,
                    keep_idx: Optional[torch.Tensor] = None, cu_out: Optional[torch.Tensor] = None,
                    status: Optional[torch.Tensor] = None, stream=None):
     """avtp_select and avtp_compact in one launch; pairs as for compact."""
@@ -318,16 +338,15 @@ def select_compact(dl: DeviceLayout, scores: torch.Tensor, budget_: torch.Tensor
         keep_idx = torch.empty(max(1, dl.N_out), dtype=torch.int32, device=dev)
     if cu_out is None:
         cu_out = torch.empty(dl.B + 1, dtype=torch.int32, device=dev)
-    descs = [tensor_desc(p[0], p[1], p[2] if len(p) > 2 else 0) for p in pairs]
-    arr = (_Tensor * max(1, len(descs)))(*descs)
+    ts = _tensor_set(pairs)
     _check(lib().avtp_select_compact(_stream(stream), dl.ref(), _ptr(scores), _ptr(budget_),
                                      _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out), _ptr(status),
-                                     arr, len(descs)), "avtp_select_compact")
+                                     ts.arr, ts.n), "avtp_select_compact")
     return keep_idx[: dl.N_out], cu_out
 
 
 def budget_select_compact(dl: DeviceLayout, img_sum: torch.Tensor, scores: torch.Tensor,
-                          pairs: Sequence, alpha: float = 1.0, lo_permille: int = 50,
+                          pairs, alpha: float = 1.0, lo_permille: int = 50,
                           hi_permille: int = 950, floor_abs: int = 0,
                           mode: int = BUDGET_PROPORTIONAL, budget_out: Optional[torch.Tensor] = None,
                           keep_idx: Optional[torch.Tensor] = None,
@@ -342,12 +361,11 @@ def budget_select_compact(dl: DeviceLayout, img_sum: torch.Tensor, scores: torch
         keep_idx = torch.empty(max(1, dl.N_out), dtype=torch.int32, device=dev)
     if cu_out is None:
         cu_out = torch.empty(dl.B + 1, dtype=torch.int32, device=dev)
-    descs = [tensor_desc(p[0], p[1], p[2] if len(p) > 2 else 0) for p in pairs]
-    arr = (_Tensor * max(1, len(descs)))(*descs)
+    ts = _tensor_set(pairs)
     _check(lib().avtp_budget_select_compact(
         _stream(stream), dl.ref(), _ptr(img_sum), mode, float(alpha), lo_permille, hi_permille,
         floor_abs, _ptr(scores), _ptr(budget_out), _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out),
-        _ptr(status), arr, len(descs)), "avtp_budget_select_compact")
+        _ptr(status), ts.arr, ts.n), "avtp_budget_select_compact")
     return budget_out[: dl.n_img], keep_idx[: dl.N_out], cu_out
 
 

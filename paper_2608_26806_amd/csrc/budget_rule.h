@@ -69,6 +69,22 @@ __device__ inline double image_weight(int n, long long M, float s32, double S, b
 constexpr int kThreads = 256;
 static_assert(kMaxImg <= kThreads, "one thread per image");
 
+// The rule's barrier: the block's (NTH = 256), or, with NTH = 64, ordering
+// among the lanes of the one wave that runs the rule (the whole block of the
+// budget kernel, or wave 0 of a selection block while the others wait): a
+// wave's LDS accesses take effect in program order, so no hardware barrier
+// is needed, only that the compiler keeps that order.
+template <int NTH>
+__device__ inline void bsync() {
+  if (NTH == 64) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __syncthreads();
+  }
+}
+
 // Block-wide sums: wave butterflies, then the four wave partials in LDS.
 template <int NTH, typename T>
 __device__ inline T block_sum(T v, T *sh) {
@@ -76,9 +92,9 @@ __device__ inline T block_sum(T v, T *sh) {
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
   if (NTH == 64) return v;
   if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
-  __syncthreads();
+  bsync<NTH>();
   const T r = sh[0] + sh[1] + sh[2] + sh[3];
-  __syncthreads();  // sh may be reused right away
+  bsync<NTH>();  // sh may be reused right away
   return r;
 }
 
@@ -107,7 +123,7 @@ __device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, ui
     shd[w] = den;
     sho[w] = ok;
   }
-  __syncthreads();
+  bsync<NTH>();
   ok = false;
   for (int t = 0; t < 4; ++t) {
     if (sho[t] && (!ok || better(shn[t], shd[t], num, den))) {
@@ -116,7 +132,7 @@ __device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, ui
       ok = true;
     }
   }
-  __syncthreads();
+  bsync<NTH>();
 }
 
 // The budgets of sequence b's images, by a block of NTH threads (every
@@ -161,13 +177,13 @@ __device__ __attribute__((always_inline)) inline void seq_budget(
   const long long M = block_sum<NTH>(n, red_i);
   const long long slo = block_sum<NTH>(l, red_i);
   const long long shi = block_sum<NTH>(h, red_i);
-  if (NTH == 64) __syncthreads();  // sv is read by thread 0 below
+  if (NTH == 64) bsync<NTH>();  // sv is read by thread 0 below
   if (tid == 0) {  // the image sum, in image order (it fixes the weights)
     double S = 0.0;
     for (int i = 0; i < m; ++i) S = S + (double)sv[i];
     sh_S = S;
   }
-  __syncthreads();
+  bsync<NTH>();
   const double S = sh_S;
   const bool good = isfinite(S) && S > 0.0;
   double w = 0.0;
@@ -178,7 +194,7 @@ __device__ __attribute__((always_inline)) inline void seq_budget(
   for (int off = 32; off > 0; off >>= 1) wmax = fmax(wmax, __shfl_xor(wmax, off));
   if (NTH > 64) {
     if ((tid & 63) == 0) red_d[tid >> 6] = wmax;
-    __syncthreads();
+    bsync<NTH>();
     wmax = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
   }
   uint64_t Wi = 0;
@@ -198,7 +214,7 @@ __device__ __attribute__((always_inline)) inline void seq_budget(
     if (tid == 0 && status) atomicOr(status + b, AVTP_FLAG_INFEASIBLE);
     return;
   }
-  __syncthreads();
+  bsync<NTH>();
 
   // Breakpoints k < m: lo_k / W_k, k >= m: hi_(k-m) / W_(k-m) (zero-length
   // images have none).  f is evaluated at every breakpoint; each thread keeps
@@ -251,7 +267,7 @@ __device__ __attribute__((always_inline)) inline void seq_budget(
       }
     }
     fpart[tid] = f;
-    __syncthreads();
+    bsync<NTH>();
     if (part == 0 && ok) {
       for (int q = 1; q < np; ++q) f += fpart[q * KB + k];
       keep_ext(f, num, den);
@@ -294,7 +310,7 @@ __device__ __attribute__((always_inline)) inline void seq_budget(
     ri = num % Q;
   }
   if (mine) rem[tid] = ri;
-  if (NTH == 64) __syncthreads();  // rem is read by every lane below
+  if (NTH == 64) bsync<NTH>();  // rem is read by every lane below
   const long long D = K - block_sum<NTH>((long long)kk, red_i);  // the units left to hand out
   // largest remainders first, lowest image index among equal ones
   if (mine) {

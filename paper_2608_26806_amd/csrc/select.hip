@@ -23,6 +23,10 @@ namespace avtp {
 namespace {
 
 constexpr int kThreads = 256;
+// most images per sequence for which wave 0 alone runs the in-block budget
+// rule (as the budget kernel does: with more, the four waves' share of the
+// breakpoint sums pays more)
+constexpr int kWaveBudgetMaxImages = 16;
 
 // Monotone map float -> uint32 (larger score -> larger key); -0.0 == +0.0,
 // NaN -> 0, below every other value.
@@ -75,35 +79,12 @@ struct RuleArgs {
   int32_t *budget;  // every image's budget is also written here (by one block)
 };
 
-// The sequence of image i (block-uniform; i < n_img).
-__device__ inline int seq_of_image(const int32_t *cu_img, int B, int i) {
-  __shared__ int sh;
-  for (int c = threadIdx.x; c < B; c += kThreads)
-    if (cu_img[c] <= i && i < cu_img[c + 1]) sh = c;
-  __syncthreads();
-  const int b = sh;
-  __syncthreads();  // (sh may be written again by the next call)
-  return b;
-}
-
-// Runs the budget rule for image i's sequence into LDS and returns the
-// matching policy.  The block with write set stores budget[i] (one block
-// per image does), and the one of the sequence's first image the
-// infeasibility flag.
-__device__ __attribute__((always_inline)) inline BudInBlock budgets_in_block(
-    const RuleArgs &R, const int32_t *img_len, const int32_t *cu_img, int B, int i, bool write,
-    int32_t *status) {
-  __shared__ int32_t bud[AVTP_MAX_IMAGES_PER_SEQ];
-  const int b = seq_of_image(cu_img, B, i);
-  const int i0 = cu_img[b];
-  budget_rule::seq_budget<kThreads>(b, R.img_sum, img_len, cu_img, R.keep_total, R.mode, R.alpha,
-                                    R.lo_pm, R.hi_pm, R.floor_abs,
-                                    write && i == i0 ? status : nullptr,
-                                    [&](int t, int32_t v) __attribute__((always_inline)) { bud[t] = v; });
-  __syncthreads();
-  if (write && threadIdx.x == 0) R.budget[i] = bud[i - i0];
-  return BudInBlock{bud, img_len, R.keep_total, b, i0};
-}
+// How a selection block gets its budgets.
+enum BudMode {
+  kBudGlobal = 0,  // from the budget kernel's output
+  kBudBlock = 1,   // the rule run by the whole block
+  kBudWave = 2,    // the rule run by wave 0 while the other waves load the image
+};
 
 // exclusive block scan of a 0/1 flag (256 threads, 4 waves); returns the
 // exclusive count and writes the block total to *total
@@ -194,15 +175,18 @@ struct SelArgs {
 
 // The kept tokens of image i (and the text rows around it), reported as
 // put(output index, token index, sequence) in no particular order.
-template <typename Put, typename Bud>
-__device__ __attribute__((always_inline)) inline void select_image(const SelArgs &A, int i, Put put,
-                                                                   const Bud &bud) {
+template <int MODE, typename Put>
+__device__ __attribute__((always_inline)) inline void select_image(const SelArgs &A,
+                                                                   const RuleArgs &R, int i,
+                                                                   bool write, int32_t *status,
+                                                                   Put put) {
   __shared__ uint32_t hist[2][256];  // double-buffered across the radix passes
   __shared__ uint32_t keys[kLdsKeys];
   __shared__ int wsum[4];
   __shared__ long long red[4];
   __shared__ uint32_t sh_digit[4];  // one slot per radix pass
-  __shared__ int sh_krem[4], sh_b;
+  __shared__ int sh_krem[4], sh_b, cnt[2];
+  __shared__ int32_t bud_sh[AVTP_MAX_IMAGES_PER_SEQ];  // the in-block budgets of b's images
   const int tid = threadIdx.x;
   const float *__restrict__ scores = A.scores;
   const int32_t *__restrict__ img_start = A.img_start;
@@ -222,33 +206,70 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
 
   for (int c = tid; c < B; c += kThreads)  // the sequence holding image i
     if (cu_img[c] <= i && i < cu_img[c + 1]) sh_b = c;
-  const int st = img_start[i], n = img_len[i];
-  const int k = bud.k(i);
-  const long long part = bud.part(i);  // (this thread's share of) the budgets of the images before i
-  // the image's order keys into LDS now: their loads overlap the prefix and
-  // text-row reductions below (whose barriers also order them before the
-  // radix passes)
-  const bool in_lds = n <= kLdsKeys;
-  if (in_lds)
-#pragma unroll 4
-    for (int j = tid; j < n; j += kThreads) keys[j] = order_key(scores[st + j]);
-  hist[0][tid] = 0;  // the first radix pass's histogram (kThreads == 256 bins)
-  const long long pre = block_sum_ll(part, red);  // (also publishes sh_b)
+  if (tid == 0) cnt[0] = cnt[1] = 0;
+  __syncthreads();
   const int b = sh_b;
+  const int st = img_start[i], n = img_len[i];
+  const bool in_lds = n <= kLdsKeys;
   const int a_lo = cu_text[b], a_hi = cu_text[b + 1];
   const bool first = i == cu_img[b], last = i + 1 == cu_img[b + 1];
-  // end of the previous image of b (an empty image may share its position
-  // with a text row, which then comes after it)
-  const int pend = first ? 0 : img_start[i - 1] + img_len[i - 1];
-  int before = 0, between = 0;  // text rows of b before the image; of those, after the previous one
-  for (int t = a_lo + tid; t < a_hi; t += kThreads) {
-    const int p = text_pos[t];
-    before += p < st;
-    between += p < st && p >= pend;
+
+  // The part that needs no budget, by threads t0 .. t0 + nt - 1 and without
+  // a block barrier: the image's order keys into LDS, the first radix
+  // pass's histogram cleared, and the text rows of b before the image (and
+  // of those, after the previous image; an empty image may share its
+  // position with a text row, which then comes after it) counted in LDS.
+  auto load_image = [&](int t0, int nt) __attribute__((always_inline)) {
+    const int u = tid - t0;
+    if (in_lds)
+#pragma unroll 4
+      for (int j = u; j < n; j += nt) keys[j] = order_key(scores[st + j]);
+    for (int x = u; x < 256; x += nt) hist[0][x] = 0;
+    const int pend = first ? 0 : img_start[i - 1] + img_len[i - 1];
+    int before = 0, between = 0;
+    for (int t = a_lo + u; t < a_hi; t += nt) {
+      const int p = text_pos[t];
+      before += p < st;
+      between += p < st && p >= pend;
+    }
+    if (before) atomicAdd(&cnt[0], before);
+    if (between) atomicAdd(&cnt[1], between);
+  };
+  // The budgets: read, or the rule run for b (while the image loads, when
+  // wave 0 runs it).  The block with write set stores budget[i], and the one
+  // of b's first image the infeasibility flag.
+  const int i0 = cu_img[b];
+  auto rule_out = [&](int t, int32_t v) __attribute__((always_inline)) { bud_sh[t] = v; };
+  int32_t *rst = write && i == i0 ? status : nullptr;
+  if constexpr (MODE == kBudWave) {
+    if (tid < 64)
+      budget_rule::seq_budget<64>(b, R.img_sum, img_len, cu_img, R.keep_total, R.mode, R.alpha,
+                                  R.lo_pm, R.hi_pm, R.floor_abs, rst, rule_out);
+    else
+      load_image(64, kThreads - 64);
+  } else if constexpr (MODE == kBudBlock) {
+    load_image(0, kThreads);  // (its loads are in flight during the rule)
+    budget_rule::seq_budget<kThreads>(b, R.img_sum, img_len, cu_img, R.keep_total, R.mode,
+                                      R.alpha, R.lo_pm, R.hi_pm, R.floor_abs, rst, rule_out);
+  } else {
+    load_image(0, kThreads);
   }
-  const long long cnt = block_sum_ll(((long long)before << 32) | (long long)between, red);
-  const int a0 = a_lo + (int)(cnt >> 32);        // first text row after the image start
-  const int am = a0 - (int)(cnt & 0xffffffffll);  // first text row after the previous image
+  __syncthreads();  // keys, histogram, counts and budgets are in LDS
+  long long part = 0;  // (this thread's share of) the budgets of the images before i
+  int k;
+  if constexpr (MODE == kBudGlobal) {
+    const BudGlobal bud{A.budget, img_len};
+    part = bud.part(i);
+    k = bud.k(i);
+  } else {
+    const BudInBlock bud{bud_sh, img_len, R.keep_total, b, i0};
+    part = bud.part(i);
+    k = bud.k(i);
+    if (write && tid == 0) R.budget[i] = bud_sh[i - i0];
+  }
+  const long long pre = block_sum_ll(part, red);
+  const int a0 = a_lo + cnt[0];  // first text row after the image start
+  const int am = a0 - cnt[1];    // first text row after the previous image
 
   // text rows between the previous image and this one, and after the last
   for (int t = am + tid; t < a0; t += kThreads) put(t + pre, text_pos[t], b);
@@ -340,9 +361,9 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   }
 }
 
-// INB: the block first runs the budget rule for its image's sequence
-// (RuleArgs) instead of reading the budget kernel's output.
-template <bool INB>
+// MODE (BudMode): kBudGlobal reads the budget kernel's output; otherwise the
+// block first runs the budget rule for its image's sequence (RuleArgs).
+template <int MODE>
 __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs A, RuleArgs R,
                                                          int32_t *__restrict__ keep_idx,
                                                          long long cap, int32_t *__restrict__ status) {
@@ -351,13 +372,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs A, RuleArgs R,
     if (o < cap) keep_idx[o] = v;
     else if (status) atomicOr(status + seq, AVTP_FLAG_OUT_CAPACITY);
   };
-  if constexpr (INB) {  // (without images select_image reads no budget)
-    select_image(A, i, put,
-                 A.n_img > 0 ? budgets_in_block(R, A.img_len, A.cu_img, A.B, i, true, status)
-                             : BudInBlock{});
-  } else {
-    select_image(A, i, put, BudGlobal{A.budget, A.img_len});
-  }
+  select_image<MODE>(A, R, i, true, status, put);
 }
 
 // Fused selection and compaction: S blocks per image (slices).  Every slice
@@ -394,7 +409,7 @@ __device__ inline void copy_listed(const CTensor &T, const int *lo, const int *l
                          });
 }
 
-template <bool INB>
+template <int MODE>
 __global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a, RuleArgs R) {
   __shared__ int list_o[kListCap], list_j[kListCap];
   __shared__ int list_n;
@@ -420,13 +435,7 @@ __global__ __launch_bounds__(kThreads) void select_compact_kernel(SCArgs a, Rule
       atomicOr(a.status + seq, AVTP_FLAG_OUT_CAPACITY);
     }
   };
-  if constexpr (INB) {
-    select_image(A, img, put,
-                 A.n_img > 0 ? budgets_in_block(R, A.img_len, A.cu_img, A.B, img, sl == 0, a.status)
-                             : BudInBlock{});
-  } else {
-    select_image(A, img, put, BudGlobal{A.budget, A.img_len});
-  }
+  select_image<MODE>(A, R, img, sl == 0, a.status, put);
   __syncthreads();
   const int n = min(list_n, kListCap);
   for (int ti = 0; ti < a.n_t; ++ti) {
@@ -486,7 +495,7 @@ hipError_t launch_select_compact(hipStream_t st, const DevLayout &L, const float
   const SCArgs a = sc_args(L, scores, budget, keep_idx, keep_capacity, cu_out, status, n_out,
                            tensors, n_tensors);
   const int images = L.n_img > 0 ? L.n_img : 1;
-  hipLaunchKernelGGL(select_compact_kernel<false>, dim3((unsigned)(images * a.S)), dim3(kThreads),
+  hipLaunchKernelGGL(select_compact_kernel<kBudGlobal>, dim3((unsigned)(images * a.S)), dim3(kThreads),
                      0, st, a, RuleArgs{});
   return hipGetLastError();
 }
@@ -497,7 +506,7 @@ hipError_t launch_select(hipStream_t st, const DevLayout &L, const float *scores
   const int grid = L.n_img > 0 ? L.n_img : 1;
   const SelArgs A{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
                   L.B, L.n_img, L.T_tot, cu_out};
-  hipLaunchKernelGGL(select_kernel<false>, dim3(grid), dim3(kThreads), 0, st, A, RuleArgs{},
+  hipLaunchKernelGGL(select_kernel<kBudGlobal>, dim3(grid), dim3(kThreads), 0, st, A, RuleArgs{},
                      keep_idx, (long long)keep_capacity, status);
   return hipGetLastError();
 }
@@ -509,9 +518,14 @@ hipError_t launch_budget_select(hipStream_t st, const DevLayout &L, const float 
   const int grid = L.n_img > 0 ? L.n_img : 1;
   const SelArgs A{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
                   L.B, L.n_img, L.T_tot, cu_out};
-  hipLaunchKernelGGL(select_kernel<true>, dim3(grid), dim3(kThreads), 0, st, A,
-                     rule_args(L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget),
-                     keep_idx, (long long)keep_capacity, status);
+  const RuleArgs R =
+      rule_args(L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget);
+  if (L.max_img_per_seq <= kWaveBudgetMaxImages)
+    hipLaunchKernelGGL(select_kernel<kBudWave>, dim3(grid), dim3(kThreads), 0, st, A, R, keep_idx,
+                       (long long)keep_capacity, status);
+  else
+    hipLaunchKernelGGL(select_kernel<kBudBlock>, dim3(grid), dim3(kThreads), 0, st, A, R,
+                       keep_idx, (long long)keep_capacity, status);
   return hipGetLastError();
 }
 
@@ -524,9 +538,13 @@ hipError_t launch_budget_select_compact(hipStream_t st, const DevLayout &L, cons
   const SCArgs a = sc_args(L, scores, budget, keep_idx, keep_capacity, cu_out, status, n_out,
                            tensors, n_tensors);
   const int images = L.n_img > 0 ? L.n_img : 1;
-  hipLaunchKernelGGL(select_compact_kernel<true>, dim3((unsigned)(images * a.S)), dim3(kThreads),
-                     0, st, a,
-                     rule_args(L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget));
+  const RuleArgs R =
+      rule_args(L, img_sum, mode, alpha, lo_permille, hi_permille, floor_abs, budget);
+  const dim3 grid((unsigned)(images * a.S));
+  if (L.max_img_per_seq <= kWaveBudgetMaxImages)
+    hipLaunchKernelGGL(select_compact_kernel<kBudWave>, grid, dim3(kThreads), 0, st, a, R);
+  else
+    hipLaunchKernelGGL(select_compact_kernel<kBudBlock>, grid, dim3(kThreads), 0, st, a, R);
   return hipGetLastError();
 }
 
