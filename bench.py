@@ -474,7 +474,9 @@ def measure_layer(wl, dev, steps, warmup):
                    reps) * 1e-3
     # the fused call and the two separate calls, timed the same way (events
     # around each call, or around the pair)
-    fused_us = _events(stream, lambda: A.select_compact(dl, scores, bud, tset, stream=sh), reps)
+    fused_us = _events(stream, lambda: A.select_compact(dl, scores, bud, tset, keep_idx=keep,
+                                                        cu_out=cu_out, status=status, stream=sh),
+                       reps)
 
     def _sep():
         A.select(dl, scores, bud, keep_idx=keep, cu_out=cu_out, status=status, stream=sh)

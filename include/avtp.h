@@ -277,7 +277,7 @@ int avtp_layer_select(avtp_stream_t stream, const float *A, int L, int N, int k,
  * tensors to n_out = T_tot + sum(keep_total) rows (the pruned subsequence of
  * Method, "Visual Token Pruning", gathered in one call).  Same arguments and
  * outputs as the two calls; the kept rows and keep_idx are bit-identical to
- * theirs.  When the compaction moves at most 32 MiB (reads plus writes) it is
+ * theirs.  When the compaction moves at most 4 MiB (reads plus writes) it is
  * one launch, for the small configurations where launches and the
  * selection's latency dominate: every image is handled by several blocks
  * that each redo its selection and copy an interleaved share of its output
@@ -303,7 +303,7 @@ int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const f
  * AVTP_ERR_INFEASIBLE.  While no sequence has more than 64 images, the
  * selection blocks each run the budget rule for their own sequence (the
  * same integer arithmetic as the budget kernel), so no budget launch is
- * needed: one launch in all when the compaction moves at most 32 MiB, else
+ * needed: one launch in all when the compaction moves at most 4 MiB, else
  * the selection and the compaction kernels.  With more images per sequence
  * the budget kernel runs first.
  * ---------------------------------------------------------------------- */

@@ -78,8 +78,9 @@ int check_attn_args(int dtype, int Hq, int Hkv, int d) {
   return AVTP_OK;
 }
 
-// avtp_select_compact: bytes moved above which it runs the two kernels
-constexpr int64_t kFusedMaxBytes = 32ll << 20;
+// avtp_select_compact, avtp_budget_select_compact: bytes moved above which
+// they run the selection and compaction kernels back to back
+constexpr int64_t kFusedMaxBytes = 4ll << 20;
 // avtp_budget_select_compact: most images per sequence for which the
 // selection blocks run the budget rule themselves
 constexpr int kInBlockBudgetMaxImages = 64;
@@ -344,9 +345,10 @@ int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const f
   // One launch pays where launches and the selection's latency dominate (few
   // bytes to move).  Every block of the fused kernel runs its image's
   // selection before it copies, so the copies cannot start before the
-  // selections end; with many bytes to move the two kernels back to back are
-  // faster (measured: config 2, 15 MB: one launch 27 us, two 31 us; config
-  // 3, 240 MB: 39 us and 34 us), and are used instead.
+  // selections end; with more bytes to move the two kernels back to back are
+  // as fast or faster (measured with events around the calls: config 1,
+  // 0.4 MB: one launch 12.2 us, two 12.8; config 2, 15 MB: 17.0 and 16.2;
+  // config 3, 240 MB: 39 and 34), and are used instead.
   const int64_t moved = bytes_moved(need, tensors, n_tensors);
   hipStream_t st = (hipStream_t)stream;
   if (moved > kFusedMaxBytes) {

@@ -106,7 +106,7 @@ def test_text_only_batch():
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
 def test_one_call_equals_separate_calls(cfg):
-    # configs 1-2 move at most 32 MiB (one launch); 3-5 more (the selection
+    # config 1 moves at most 4 MiB (one launch); 2-5 more (the selection
     # blocks with in-block budgets, then the compaction kernel)
     wl = make_workload(cfg, payload=True)
     lay = wl.layout
