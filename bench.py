@@ -493,6 +493,35 @@ def measure_layer(wl, dev, steps, warmup):
 
     lse_layer_us = _events(stream, _layer_lse, reps)
 
+    # the same step captured once in a HIP graph and replayed (no host work
+    # per call): what the layer costs the GPU alone, beside the eager steps
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        score_attn_cur = lambda: A.score_attn(dl, q, k, wl.softmax_scale, scores=scores,
+                                              img_sum=isum, status=status, ws=ws)
+        prune_cur = lambda: A.budget_select_compact(dl, isum, scores, tset, *bargs, budget_out=bud,
+                                                    keep_idx=keep, cu_out=cu_out, status=status)
+        score_attn_cur()
+        prune_cur()
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        score_attn_cur()
+        prune_cur()
+    torch.cuda.synchronize()
+    graph.replay()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    g0.record(stream)
+    for _ in range(steps):  # back to back, as the timed steps
+        graph.replay()
+    g1.record(stream)
+    torch.cuda.synchronize()
+    graph_us = g0.elapsed_time(g1) / steps * 1e3
+    del graph
+
     M = int(lay.img_len.sum())
     ms = {n: float(np.mean(per[:, j])) for j, n in enumerate(names)}
     ms_score = float(np.mean(per2[:, 0]))
@@ -524,6 +553,7 @@ def measure_layer(wl, dev, steps, warmup):
                              "alg_bytes": comp_bytes},
         "select_plus_compact_hbm_frac": selcomp_gbs / PEAK_HBM_GBS,
         "layer_with_supplied_lse_us": lse_layer_us,
+        "layer_graph_replay_us": graph_us,
         "select_compact_fused": {
             "us": fused_us,
             "hbm_frac": (comp_bytes + sel_bytes) / (fused_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
@@ -641,6 +671,7 @@ def main():
         "roofline_compact": rep["roofline_compact"],
         "select_plus_compact_hbm_frac": rep["select_plus_compact_hbm_frac"],
         "layer_with_supplied_lse_us": rep["layer_with_supplied_lse_us"],
+        "layer_graph_replay_us": rep["layer_graph_replay_us"],
         "select_compact_fused": rep["select_compact_fused"],
         "layer_selection": layer_sel,
         "variation_and_progressive": var_prog,
