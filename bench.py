@@ -368,8 +368,9 @@ def measure_layer(wl, dev, steps, warmup):
 
     The timed step is two calls of the C ABI: avtp_score in its plain
     two-pass form, then avtp_budget_select_compact (budgets, selection and
-    the compaction of hidden states, position ids, K and V); the `steps`
-    steps are timed together, one HIP event pair around them.  Loops of
+    the compaction of hidden states, position ids, K and V), each prepared
+    once by the binding (arguments marshalled once); the `steps` steps are
+    timed together, one HIP event pair around them.  Loops of
     their own, events between the calls, give the split between the two
     calls and the same layer as four calls (avtp_score, avtp_budget,
     avtp_select, avtp_compact) for the per-stage breakdown.  Pass 1 alone (avtp_row_lse: row statistics
@@ -413,10 +414,10 @@ def measure_layer(wl, dev, steps, warmup):
     score_call = lambda: A.score_attn(dl, q, k, wl.softmax_scale, scores=scores, img_sum=isum,
                                       status=status, ws=ws, stream=sh)
     bargs = (wl.alpha, wl.lo_permille, wl.hi_permille, wl.floor_abs)
-    calls = [  # the timed step
-        score_call,
-        lambda: A.budget_select_compact(dl, isum, scores, tset, *bargs, budget_out=bud,
-                                        keep_idx=keep, cu_out=cu_out, status=status, stream=sh),
+    calls = [  # the timed step: the two calls with their arguments marshalled once
+        A.prepare_score_attn(dl, q, k, wl.softmax_scale, scores, isum, ws, status=status, stream=sh),
+        A.prepare_budget_select_compact(dl, isum, scores, tset, bud, keep, cu_out, *bargs,
+                                        status=status, stream=sh),
     ]
     names = ["score", "budget", "select", "compact"]
     calls4 = [  # the same layer as four calls

@@ -203,6 +203,49 @@ def row_lse(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor, softmax_sca
     return out
 
 
+class Prepared:
+    """One C ABI call with its arguments marshalled once: calling it issues the
+    call again on the same buffers (for loops that repeat a call, where the
+    per-call Python work would otherwise be a large part of a small layer's
+    time).  It keeps the objects the arguments point into alive."""
+
+    def __init__(self, fn, args: tuple, where: str, keep: tuple):
+        self._fn, self._args, self._where, self._keep = fn, args, where, keep
+
+    def __call__(self) -> None:
+        rc = self._fn(*self._args)
+        if rc != OK:
+            raise AvtpError(rc, self._where)
+
+
+def prepare_score_attn(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor,
+                       softmax_scale: float, scores: torch.Tensor, img_sum: torch.Tensor,
+                       ws: torch.Tensor, row_lse: Optional[torch.Tensor] = None,
+                       status: Optional[torch.Tensor] = None, stream=None) -> Prepared:
+    """avtp_score (attention mode) on fixed buffers, as a Prepared call."""
+    T, Hq, d = q_text.shape
+    args = (_stream(stream), dl.ref(), SCORE_ATTN, dtype_code(q_text), _ptr(q_text), _ptr(k), Hq,
+            k.shape[1], d, float(softmax_scale), _ptr(row_lse), None, None, 0, _ptr(scores),
+            _ptr(img_sum), _ptr(status), _ptr(ws), ws.numel())
+    return Prepared(lib().avtp_score, args, "avtp_score",
+                    (dl, q_text, k, scores, img_sum, ws, row_lse, status, stream))
+
+
+def prepare_budget_select_compact(dl: DeviceLayout, img_sum: torch.Tensor, scores: torch.Tensor,
+                                  pairs, budget_out: torch.Tensor, keep_idx: torch.Tensor,
+                                  cu_out: torch.Tensor, alpha: float = 1.0, lo_permille: int = 50,
+                                  hi_permille: int = 950, floor_abs: int = 0,
+                                  mode: int = BUDGET_PROPORTIONAL,
+                                  status: Optional[torch.Tensor] = None, stream=None) -> Prepared:
+    """avtp_budget_select_compact on fixed buffers, as a Prepared call."""
+    ts = _tensor_set(pairs)
+    args = (_stream(stream), dl.ref(), _ptr(img_sum), mode, float(alpha), lo_permille, hi_permille,
+            floor_abs, _ptr(scores), _ptr(budget_out), _ptr(keep_idx), keep_idx.numel(),
+            _ptr(cu_out), _ptr(status), ts.arr, ts.n)
+    return Prepared(lib().avtp_budget_select_compact, args, "avtp_budget_select_compact",
+                    (dl, img_sum, scores, ts, budget_out, keep_idx, cu_out, status, stream))
+
+
 def score_attn(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor, softmax_scale: float,
                row_lse: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
                img_sum: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,

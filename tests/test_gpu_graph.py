@@ -7,7 +7,8 @@ and they allocate nothing and enqueue no memset, so they can be captured.
 Each replay follows eager work that overwrites every output, and each
 replay's outputs (scores, image sums, budgets, kept indices, cu_out, the
 compacted hidden states, position ids, K and V, status) must equal the eager
-step's bit for bit."""
+step's bit for bit.  The binding's prepared calls (arguments marshalled once,
+as the bench's timed step issues them) are checked the same way."""
 import numpy as np
 import pytest
 import torch
@@ -97,6 +98,29 @@ def test_graph_replays_equal_the_eager_step(cfg, noalloc):
         _scramble(out)
         torch.cuda.synchronize()
         g.replay()
+        torch.cuda.synchronize()
+        for n, t in out.items():
+            assert np.array_equal(to_host_bits(t), ref[n]), (r, n)
+
+
+def test_prepared_calls_equal_the_plain_calls():
+    # the binding's prepared calls (arguments marshalled once), issued twice,
+    # against the plain calls on the same inputs
+    wl, dl, q, k, ws, out, tset = _setup(2)
+    say("[prepared] config 2")
+    _scramble(out)
+    _step(wl, dl, q, k, ws, out, tset, False)
+    torch.cuda.synchronize()
+    ref = {n: to_host_bits(t) for n, t in out.items()}
+    calls = [A.prepare_score_attn(dl, q, k, wl.softmax_scale, out["scores"], out["isum"], ws,
+                                  status=out["status"]),
+             A.prepare_budget_select_compact(dl, out["isum"], out["scores"], tset, out["bud"],
+                                             out["keep"], out["cu_out"], wl.alpha, wl.lo_permille,
+                                             wl.hi_permille, wl.floor_abs, status=out["status"])]
+    for r in range(2):
+        _scramble(out)
+        for c in calls:
+            c()
         torch.cuda.synchronize()
         for n, t in out.items():
             assert np.array_equal(to_host_bits(t), ref[n]), (r, n)
