@@ -27,6 +27,7 @@
 #include <stdint.h>
 
 #include "avtp_internal.h"
+#include "wave_ops.h"
 
 namespace avtp {
 namespace budget_rule {
@@ -85,11 +86,11 @@ __device__ inline void bsync() {
   }
 }
 
-// Block-wide sums: wave butterflies, then the four wave partials in LDS.
+// Block-wide sums: wave all-reductions (integer sums, exact in any order),
+// then the four wave partials in LDS.
 template <int NTH, typename T>
 __device__ inline T block_sum(T v, T *sh) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  v = wave::sum(v);
   if (NTH == 64) return v;
   if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
   bsync<NTH>();
@@ -97,6 +98,20 @@ __device__ inline T block_sum(T v, T *sh) {
   bsync<NTH>();  // sh may be reused right away
   return r;
 }
+
+// A fraction num/den and whether it is set, as a value of wave::allreduce.
+struct Frac {
+  uint64_t n, d;
+  uint32_t ok;
+  template <int CTRL>
+  __device__ static Frac shift(const Frac &a) {
+    return Frac{wave::dpp<CTRL>(a.n), wave::dpp<CTRL>(a.d), wave::dpp<CTRL>(a.ok)};
+  }
+  __device__ static Frac at(const Frac &a, int lane) {
+    return Frac{wave::lane_value(a.n, lane), wave::lane_value(a.d, lane),
+                wave::lane_value(a.ok, lane)};
+  }
+};
 
 // Block-wide extreme of fractions num/den (den > 0) among the threads with
 // ok set: the smallest (MIN) or the largest.  Returns ok = false if none.
@@ -106,16 +121,14 @@ __device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, ui
   auto better = [](uint64_t an, uint64_t ad, uint64_t bn, uint64_t bd) {
     return MIN ? frac_lt(an, ad, bn, bd) : frac_lt(bn, bd, an, ad);
   };
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const uint64_t on = __shfl_xor(num, off), od = __shfl_xor(den, off);
-    const bool oo = __shfl_xor((int)ok, off) != 0;
-    if (oo && (!ok || better(on, od, num, den))) {
-      num = on;
-      den = od;
-      ok = true;
-    }
-  }
+  // the wave's extreme: a choice by exact comparison, so equal fractions in
+  // any form give the same value whichever is kept
+  const Frac f = wave::allreduce(Frac{num, den, ok ? 1u : 0u}, [&](Frac a, Frac b) {
+    return (b.ok && (!a.ok || better(b.n, b.d, a.n, a.d))) ? b : a;
+  });
+  num = f.n;
+  den = f.d;
+  ok = f.ok != 0;
   if (NTH == 64) return;
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
@@ -189,9 +202,7 @@ __device__ __attribute__((always_inline)) inline void seq_budget(
   double w = 0.0;
   if (mine) w = image_weight((int)n, M, s32, S, good, mode, (double)alpha, (int)K);
   // the largest weight (weights are >= 0; images without tokens have none)
-  double wmax = w;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) wmax = fmax(wmax, __shfl_xor(wmax, off));
+  double wmax = wave::max(w);
   if (NTH > 64) {
     if ((tid & 63) == 0) red_d[tid >> 6] = wmax;
     bsync<NTH>();

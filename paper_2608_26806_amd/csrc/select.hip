@@ -18,6 +18,7 @@
 #include "avtp_internal.h"
 #include "budget_rule.h"
 #include "row_copy.h"
+#include "wave_ops.h"
 
 namespace avtp {
 namespace {
@@ -104,12 +105,7 @@ __device__ inline int block_scan_flag(bool f, int *wsum, int *total) {
 // exclusive block scan of an integer (256 threads); block total in *total
 __device__ inline int block_scan_int(int v, int *wsum, int *total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int inc = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int u = __shfl_up(inc, off);
-    if (lane >= off) inc += u;
-  }
+  const int inc = (int)wave::prefix_sum((uint32_t)v);  // (v >= 0)
   if (lane == 63) wsum[wave] = inc;
   __syncthreads();
   int off = 0;
@@ -121,8 +117,7 @@ __device__ inline int block_scan_int(int v, int *wsum, int *total) {
 
 // block-wide sum of a 64-bit value
 __device__ inline long long block_sum_ll(long long v, long long *sh) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  v = wave::sum(v);
   if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
   __syncthreads();
   const long long r = sh[0] + sh[1] + sh[2] + sh[3];
@@ -136,15 +131,13 @@ constexpr int kLdsKeys = 4096;  // images up to this length keep their keys in L
 // a 256-bin histogram of byte `shift`; updates krem to the rank inside the bin.
 __device__ inline void pick_digit(const uint32_t *hist, int krem, uint32_t *sh_digit, int *sh_krem) {
   if (threadIdx.x < 64) {
-    // lane owns bins 4*lane .. 4*lane+3; suffix sums over lanes (high bins first)
-    const int lane = threadIdx.x;
-    const int c = hist[4 * lane] + hist[4 * lane + 1] + hist[4 * lane + 2] + hist[4 * lane + 3];
-    int suf = c;
-    for (int off = 1; off < 64; off <<= 1) {
-      const int v = __shfl_down(suf, off);
-      if (lane + off < 64) suf += v;
-    }
-    const int above = suf - c;  // keys in bins of higher lanes
+    // lane l owns bins 4*o .. 4*o+3 with o = 63 - l, so that a prefix sum
+    // over the lanes is the sum over the bins from the highest down to its own
+    const int o = 63 - (int)threadIdx.x;
+    const int c = hist[4 * o] + hist[4 * o + 1] + hist[4 * o + 2] + hist[4 * o + 3];
+    const int suf = (int)wave::prefix_sum((uint32_t)c);
+    const int above = suf - c;  // keys in higher bins
+    const int lane = o;
     if (suf >= krem && above < krem) {
       int acc = above;
       for (int x = 4 * lane + 3; x >= 4 * lane; --x) {
