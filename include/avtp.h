@@ -71,6 +71,11 @@ typedef enum {
 #define AVTP_MAX_TENSORS 8
 #define AVTP_MAX_LAYERS 1024       /* avtp_layer_select: layers               */
 #define AVTP_MAX_SAMPLES (1 << 20) /* avtp_layer_select: samples              */
+/* The attention score (avtp_score in attention mode, avtp_row_lse) addresses
+ * one sequence's keys and text-row queries with 32-bit byte offsets: every
+ * sequence must have (its tokens) * Hkv * d * elem and (its text rows) *
+ * Hq * d * elem below AVTP_MAX_SEQ_BYTES (elem: 2 for bf16, 4 for fp32). */
+#define AVTP_MAX_SEQ_BYTES (1ll << 32)
 
 /*
  * Packed ("THD") description of one batch of B sequences, N_tok tokens.

@@ -78,6 +78,16 @@ int check_attn_args(int dtype, int Hq, int Hkv, int d) {
   return AVTP_OK;
 }
 
+// The score kernels address a sequence's keys (from its first token) and its
+// text-row queries (from its first text row) with 32-bit byte offsets.
+int check_attn_extent(const DevLayout &L, int dtype, int Hq, int Hkv, int d) {
+  const long long row = (long long)d * (dtype == AVTP_FP32 ? 4 : 2);
+  if ((long long)L.max_seqlen * Hkv * row >= AVTP_MAX_SEQ_BYTES ||
+      (long long)L.max_text * Hq * row >= AVTP_MAX_SEQ_BYTES)
+    return AVTP_ERR_UNSUPPORTED;
+  return AVTP_OK;
+}
+
 // avtp_select_compact, avtp_budget_select_compact: bytes moved above which
 // they run the selection and compaction kernels back to back
 constexpr int64_t kFusedMaxBytes = 4ll << 20;
@@ -117,7 +127,9 @@ size_t avtp_score_workspace_size(const avtp_layout *layout, int mode, int dtype,
   DevLayout L;
   if (check_layout(layout, &L) != AVTP_OK) return 0;
   if (mode == AVTP_SCORE_VARIATION) return variation_workspace_bytes(L);
-  if (mode != AVTP_SCORE_ATTN || check_attn_args(dtype, Hq, Hkv, d) != AVTP_OK) return 0;
+  if (mode != AVTP_SCORE_ATTN || check_attn_args(dtype, Hq, Hkv, d) != AVTP_OK ||
+      check_attn_extent(L, dtype, Hq, Hkv, d) != AVTP_OK)
+    return 0;
   return attn_plan(L, Hq, Hkv, d, dtype).bytes;
 }
 
@@ -128,6 +140,7 @@ int avtp_row_lse(avtp_stream_t stream, const avtp_layout *layout, int dtype, con
   int rc = check_layout(layout, &L);
   if (rc != AVTP_OK) return rc;
   if ((rc = check_attn_args(dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
+  if ((rc = check_attn_extent(L, dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
   if (!q_text || !k || !row_lse_out || !(std::isfinite(softmax_scale)) || softmax_scale <= 0.f)
     return AVTP_ERR_INVALID_ARG;
   if ((uintptr_t)q_text % 16 || (uintptr_t)k % 16) return AVTP_ERR_INVALID_ARG;
@@ -168,6 +181,7 @@ int score_impl(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
   }
   if (mode != AVTP_SCORE_ATTN) return AVTP_ERR_INVALID_ARG;
   if ((rc = check_attn_args(dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
+  if ((rc = check_attn_extent(L, dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
   if (!q_text || !k || !(std::isfinite(softmax_scale)) || softmax_scale <= 0.f)
     return AVTP_ERR_INVALID_ARG;
   if ((uintptr_t)q_text % 16 || (uintptr_t)k % 16 || (row_lse && (uintptr_t)row_lse % 4))

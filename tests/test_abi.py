@@ -211,6 +211,31 @@ def test_budget_select_compact_arguments_rejected_on_host():
     assert f(None, dl.ref(), *args) == A.ERR_INVALID_ARG          # null src
 
 
+def test_score_rejects_sequences_past_the_32bit_offset_range():
+    """The score kernels address a sequence's keys and text-row queries with
+    32-bit byte offsets; longer sequences are rejected on the host."""
+    lib = A.lib()
+    buf = torch.zeros(1 << 16, dtype=torch.uint8)
+    p = ctypes.c_void_p(buf.data_ptr())
+    big = _dl(build_layout([[300000]], 0, 10, 10))    # 300,010 tokens
+
+    def call(dl, Hq, Hkv, ws_bytes=1 << 16):
+        return lib.avtp_score(None, dl.ref(), A.SCORE_ATTN, A.BF16, p, p, Hq, Hkv, 128, 0.1, None,
+                              None, None, 0, p, p, None, p, ws_bytes)
+
+    # keys: 300,010 * 64 heads * 256 B = 4.9 GB >= 4 GiB
+    assert call(big, 64, 64) == A.ERR_UNSUPPORTED
+    assert A.score_workspace_bytes(big, A.SCORE_ATTN, A.BF16, 64, 64, 128) == 0
+    assert lib.avtp_row_lse(None, big.ref(), A.BF16, p, p, 64, 64, 128, 0.1, p, p, 1 << 16) \
+        == A.ERR_UNSUPPORTED
+    # 8 key heads: 614 MB, accepted (then the workspace is too small)
+    assert A.score_workspace_bytes(big, A.SCORE_ATTN, A.BF16, 64, 8, 128) > (1 << 16)
+    assert call(big, 64, 8) == A.ERR_WORKSPACE
+    # text-row queries: 70,000 rows * 256 heads * 256 B = 4.6 GB
+    text = _dl(build_layout([[16]], 0, 70000, 10))
+    assert call(text, 256, 8) == A.ERR_UNSUPPORTED
+
+
 def test_noalloc_rejects_oversize_and_bad_args_on_the_host():
     """avtp_score_noalloc checks every argument, and that the layout fits its
     scratch, before any HIP call (so this runs without a GPU)."""
