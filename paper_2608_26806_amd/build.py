@@ -18,8 +18,8 @@ LIB = os.path.join(HERE, "libavtp.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["avtp_api.cpp", "score_attn.hip", "score_variation.hip", "budget.hip", "select.hip",
-           "compact.hip", "layer_stat.hip", "progressive.hip", "score_noalloc.hip"]
+SOURCES = ["avtp_api.cpp", "score_attn.hip", "finalize.hip", "score_variation.hip", "budget.hip",
+           "select.hip", "compact.hip", "layer_stat.hip", "progressive.hip", "score_noalloc.hip"]
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          # packed fp32 ALU ops stay off on this target

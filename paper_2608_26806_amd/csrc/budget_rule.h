@@ -113,39 +113,45 @@ struct Frac {
   }
 };
 
-// Block-wide extreme of fractions num/den (den > 0) among the threads with
-// ok set: the smallest (MIN) or the largest.  Returns ok = false if none.
-template <bool MIN, int NTH>
-__device__ inline void block_frac_ext(uint64_t &num, uint64_t &den, bool &ok, uint64_t *shn,
-                                      uint64_t *shd, int *sho) {
-  auto better = [](uint64_t an, uint64_t ad, uint64_t bn, uint64_t bd) {
-    return MIN ? frac_lt(an, ad, bn, bd) : frac_lt(bn, bd, an, ad);
-  };
-  // the wave's extreme: a choice by exact comparison, so equal fractions in
-  // any form give the same value whichever is kept
-  const Frac f = wave::allreduce(Frac{num, den, ok ? 1u : 0u}, [&](Frac a, Frac b) {
-    return (b.ok && (!a.ok || better(b.n, b.d, a.n, a.d))) ? b : a;
-  });
-  num = f.n;
-  den = f.d;
-  ok = f.ok != 0;
-  if (NTH == 64) return;
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    shn[w] = num;
-    shd[w] = den;
-    sho[w] = ok;
+// Block-wide extremes of two sets of fractions num/den (den > 0), each among
+// the threads with its ok set: the smallest of the first set (bn/bd, hn) and
+// the largest of the second (pn/pd, hp), in one pass.  ok = false if none.
+// The choice is by exact comparison, so equal fractions in any form give the
+// same value whichever is kept.
+struct Frac2 {
+  Frac lo, hi;
+  template <int CTRL>
+  __device__ static Frac2 shift(const Frac2 &a) {
+    return Frac2{Frac::shift<CTRL>(a.lo), Frac::shift<CTRL>(a.hi)};
   }
-  bsync<NTH>();
-  ok = false;
-  for (int t = 0; t < 4; ++t) {
-    if (sho[t] && (!ok || better(shn[t], shd[t], num, den))) {
-      num = shn[t];
-      den = shd[t];
-      ok = true;
-    }
+  __device__ static Frac2 at(const Frac2 &a, int lane) {
+    return Frac2{Frac::at(a.lo, lane), Frac::at(a.hi, lane)};
   }
-  bsync<NTH>();
+};
+__device__ inline Frac2 frac_ext_combine(const Frac2 &a, const Frac2 &b) {
+  Frac2 r = a;
+  if (b.lo.ok && (!a.lo.ok || frac_lt(b.lo.n, b.lo.d, a.lo.n, a.lo.d))) r.lo = b.lo;
+  if (b.hi.ok && (!a.hi.ok || frac_lt(a.hi.n, a.hi.d, b.hi.n, b.hi.d))) r.hi = b.hi;
+  return r;
+}
+template <int NTH>
+__device__ inline void block_frac_ext2(uint64_t &bn, uint64_t &bd, bool &hn, uint64_t &pn,
+                                       uint64_t &pd, bool &hp, Frac2 *sh) {
+  Frac2 f = wave::allreduce(Frac2{Frac{bn, bd, hn ? 1u : 0u}, Frac{pn, pd, hp ? 1u : 0u}},
+                            frac_ext_combine);
+  if (NTH > 64) {
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = f;
+    bsync<NTH>();
+    f = sh[0];
+    for (int t = 1; t < 4; ++t) f = frac_ext_combine(f, sh[t]);
+    bsync<NTH>();
+  }
+  bn = f.lo.n;
+  bd = f.lo.d;
+  hn = f.lo.ok != 0;
+  pn = f.hi.n;
+  pd = f.hi.d;
+  hp = f.hi.ok != 0;
 }
 
 // The budgets of sequence b's images, by a block of NTH threads (every
@@ -163,8 +169,8 @@ __device__ __attribute__((always_inline)) inline void seq_budget(
   __shared__ int32_t lo[kMaxImg], hi[kMaxImg];
   __shared__ float sv[kMaxImg];
   __shared__ long long red_i[4];
-  __shared__ uint64_t red_u[4], ext_n[4], ext_d[4];
-  __shared__ int ext_o[4];
+  __shared__ uint64_t red_u[4];
+  __shared__ Frac2 ext[4];
   __shared__ double sh_S, red_d[4];
 
   const int tid = threadIdx.x;
@@ -291,8 +297,7 @@ __device__ __attribute__((always_inline)) inline void seq_budget(
       keep_ext(partial_f(num, den, 0, m), num, den);
     }
   }
-  block_frac_ext<true, NTH>(bn, bd, hn, ext_n, ext_d, ext_o);
-  block_frac_ext<false, NTH>(pn, pd, hp, ext_n, ext_d, ext_o);
+  block_frac_ext2<NTH>(bn, bd, hn, pn, pd, hp, ext);
 
   // classify the images on the segment (prev, next]: pinned at lo, at hi, or free
   int32_t kk = 0;

@@ -4,9 +4,10 @@
 // (ds_bpermute) at every step; here the lanes of a quad are combined with
 // quad permutes, the four quads of each 16-lane row with two row rotates,
 // and the four rows by reading one lane of each (v_readlane), so the result
-// is wave-uniform.  The operation must be associative and commutative, and
-// exact for the results to be independent of the combining order (integer
-// sums, max / min, or a choice by an exact comparison): every caller here is.
+// is wave-uniform.  The operation must be associative and commutative.  The
+// combining pattern is fixed, so results are the same on every run; integer
+// sums, max / min and choices by exact comparison are also independent of
+// it, while a floating-point sum rounds in this pattern's order.
 #pragma once
 
 #include <hip/hip_runtime.h>
