@@ -3,12 +3,13 @@
 // with h the hidden state at the pruning layer and h' the state saved after
 // the previous pruning (the input embeddings before the first one).
 // HBM-bound: one wave streams both rows of a token with 16-byte loads and
-// reduces the three fp32 sums with a fixed butterfly.
+// reduces the three fp32 sums over its lanes in a fixed order.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
 
 #include "avtp_internal.h"
+#include "wave_ops.h"
 
 namespace avtp {
 namespace {
@@ -45,6 +46,22 @@ __device__ inline void acc8(const uint4 &x, const uint4 &y, float &dot, float &n
   }
 }
 
+// three fp32 sums, as a value of wave::allreduce
+struct Sums3 {
+  float a, b, c;
+  template <int CTRL>
+  __device__ static Sums3 shift(const Sums3 &v) {
+    return Sums3{__uint_as_float(wave::dpp<CTRL>(__float_as_uint(v.a))),
+                 __uint_as_float(wave::dpp<CTRL>(__float_as_uint(v.b))),
+                 __uint_as_float(wave::dpp<CTRL>(__float_as_uint(v.c)))};
+  }
+  __device__ static Sums3 at(const Sums3 &v, int lane) {
+    return Sums3{__uint_as_float(wave::lane_value(__float_as_uint(v.a), lane)),
+                 __uint_as_float(wave::lane_value(__float_as_uint(v.b), lane)),
+                 __uint_as_float(wave::lane_value(__float_as_uint(v.c), lane))};
+  }
+};
+
 template <typename T>
 __global__ __launch_bounds__(256) void variation_kernel(const char *__restrict__ hc,
                                                         const char *__restrict__ hp, int hidden,
@@ -66,13 +83,11 @@ __global__ __launch_bounds__(256) void variation_kernel(const char *__restrict__
     const uint4 *b = reinterpret_cast<const uint4 *>(hp + row * row_bytes);
     float dot = 0.f, nx = 0.f, ny = 0.f;
     for (int v = lane; v < nvec; v += 64) acc8(a[v], b[v], dot, nx, ny, (T *)nullptr);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      dot += __shfl_xor(dot, off);
-      nx += __shfl_xor(nx, off);
-      ny += __shfl_xor(ny, off);
-    }
-    if (lane == 0) scores[row] = 1.f - dot / fmaxf(sqrtf(nx) * sqrtf(ny), 1e-8f);
+    // the three sums over the wave in a fixed order (DPP lane network)
+    const Sums3 r = wave::allreduce(Sums3{dot, nx, ny}, [](const Sums3 &x, const Sums3 &y) {
+      return Sums3{x.a + y.a, x.b + y.b, x.c + y.c};
+    });
+    if (lane == 0) scores[row] = 1.f - r.a / fmaxf(sqrtf(r.b) * sqrtf(r.c), 1e-8f);
   }
 }
 
