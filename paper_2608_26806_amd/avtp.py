@@ -427,12 +427,16 @@ def compact_new(dl: DeviceLayout, keep_idx: torch.Tensor, srcs: Sequence, stream
 
 # --------------------------------------------------------------------------- progressive pruning
 def pruned_layout(dl: DeviceLayout, keep_idx: torch.Tensor, cu_out: torch.Tensor,
-                  stream=None) -> dict:
-    """Device arrays of the next pruning layer's layout (all but keep_total)."""
+                  stream=None, out: Optional[dict] = None) -> dict:
+    """Device arrays of the next pruning layer's layout (all but keep_total).
+    out: the six int32 arrays to write (as returned by an earlier call on the
+    same layout), else they are allocated."""
     dev = cu_out.device
-    out = {n: torch.empty(max(1, m), dtype=torch.int32, device=dev)
-           for n, m in (("cu_seqlens", dl.B + 1), ("img_start", dl.n_img), ("img_len", dl.n_img),
-                        ("cu_img", dl.B + 1), ("text_pos", dl.T_tot), ("cu_text", dl.B + 1))}
+    if out is None:
+        out = {n: torch.empty(max(1, m), dtype=torch.int32, device=dev)
+               for n, m in (("cu_seqlens", dl.B + 1), ("img_start", dl.n_img),
+                            ("img_len", dl.n_img), ("cu_img", dl.B + 1), ("text_pos", dl.T_tot),
+                            ("cu_text", dl.B + 1))}
     _check(lib().avtp_pruned_layout(_stream(stream), dl.ref(), _ptr(keep_idx), _ptr(cu_out),
                                     *[_ptr(out[n]) for n in ("cu_seqlens", "img_start", "img_len",
                                                              "cu_img", "text_pos", "cu_text")]),

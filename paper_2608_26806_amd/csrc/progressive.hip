@@ -15,8 +15,8 @@
 namespace avtp {
 namespace {
 
-// number of entries of the ascending list [lo, hi) below p
-__device__ inline int count_below(const int32_t *__restrict__ lo, int n, int32_t p) {
+// number of entries of the ascending list lo[0 .. n) below p
+__device__ inline int count_below(const int32_t *lo, int n, int32_t p) {
   int a = 0, b = n;
   while (a < b) {
     const int m = (a + b) >> 1;
@@ -27,8 +27,12 @@ __device__ inline int count_below(const int32_t *__restrict__ lo, int n, int32_t
 }
 
 constexpr int kThreads = 256;
+constexpr int kLdsKept = 16384;  // kept lists up to this long are searched in LDS
 
-// One block per sequence: its images and text rows, and its offsets.
+// One block per sequence: its images and text rows, and its offsets.  The
+// sequence's kept list is first copied to LDS (one coalesced pass), so that
+// the binary searches' dependent reads are LDS reads; a longer list is
+// searched in place.
 __global__ __launch_bounds__(kThreads) void pruned_layout_kernel(
     const int32_t *__restrict__ img_start, const int32_t *__restrict__ img_len,
     const int32_t *__restrict__ cu_img, const int32_t *__restrict__ text_pos,
@@ -37,17 +41,27 @@ __global__ __launch_bounds__(kThreads) void pruned_layout_kernel(
     int32_t *__restrict__ img_start_out, int32_t *__restrict__ img_len_out,
     int32_t *__restrict__ cu_img_out, int32_t *__restrict__ text_pos_out,
     int32_t *__restrict__ cu_text_out) {
+  __shared__ int32_t kept_sh[kLdsKept];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int o0 = cu_out[b], n = cu_out[b + 1] - o0;
   const int32_t *kept = keep_idx + o0;
-  for (int i = cu_img[b] + tid; i < cu_img[b + 1]; i += kThreads) {
-    const int s = count_below(kept, n, img_start[i]);
-    const int e = count_below(kept, n, img_start[i] + img_len[i]);
-    img_start_out[i] = o0 + s;
-    img_len_out[i] = e - s;
+  auto positions = [&](const int32_t *list) __attribute__((always_inline)) {
+    for (int i = cu_img[b] + tid; i < cu_img[b + 1]; i += kThreads) {
+      const int s = count_below(list, n, img_start[i]);
+      const int e = count_below(list, n, img_start[i] + img_len[i]);
+      img_start_out[i] = o0 + s;
+      img_len_out[i] = e - s;
+    }
+    for (int t = cu_text[b] + tid; t < cu_text[b + 1]; t += kThreads)
+      text_pos_out[t] = o0 + count_below(list, n, text_pos[t]);
+  };
+  if (n <= kLdsKept) {  // (block-uniform)
+    for (int j = tid; j < n; j += kThreads) kept_sh[j] = kept[j];
+    __syncthreads();
+    positions(kept_sh);
+  } else {
+    positions(kept);
   }
-  for (int t = cu_text[b] + tid; t < cu_text[b + 1]; t += kThreads)
-    text_pos_out[t] = o0 + count_below(kept, n, text_pos[t]);
   if (tid == 0) {
     cu_seqlens_out[b + 1] = cu_out[b + 1];
     cu_img_out[b + 1] = cu_img[b + 1];

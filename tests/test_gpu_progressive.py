@@ -30,6 +30,9 @@ LAYOUTS = {
     "mixed": ([[300, 1, 57], [], [129, 64, 2]], 4, 9),
     "gaps": ([[0, 5], [9000, 3], [], [50, 0, 7]], 0, 6),
     "one": ([[33]], 1, 1),
+    # a sequence keeping more than the 16,384 entries the kernel searches in
+    # LDS (searched in place) beside one that fits
+    "long": ([[60000, 7], [500]], 2, 3),
 }
 
 
