@@ -64,11 +64,12 @@ struct Mma<float> {
 
 // Register budget, two waves per SIMD (256 VGPRs per wave).  Pass 1 keeps
 // two 32-row query tiles per wave and four accumulator sets; pass 2 keeps up
-// to 96 registers of stationary key tiles, one accumulator set each.
+// to 96 registers of stationary key tiles, one accumulator set each.  fp32
+// operands at d = 128 do not fit that budget and run one wave per SIMD.
 constexpr int kTiles1 = 2;
-template <typename T>
-struct Occ1 {
-  static constexpr int value = 2;
+template <typename T, int D>
+struct Occ {
+  static constexpr int value = (sizeof(T) == 4 && D == 128) ? 1 : 2;
 };
 // pass 2: stationary key fragments take at most 96 registers
 __host__ __device__ constexpr int tiles_pass2(int row_bytes) {
@@ -276,7 +277,7 @@ struct P1Args {
 // token-major (the G heads of one text token adjacent), so a block's rows
 // span few positions and a block of early text rows stops at its last row.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, Occ1<T>::value) void rowstats_kernel(P1Args a) {
+__global__ __launch_bounds__(kThreads, (Occ<T, D>::value)) void rowstats_kernel(P1Args a) {
   using G_ = Geo<T, D>;
   using MM = Mma<T>;
   using frag = typename MM::frag;
@@ -692,7 +693,7 @@ struct P2Args {
 // which see only part of the wave's keys is done unpipelined with a
 // per-element mask; sub-tiles that see none are skipped.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void colsum_kernel(P2Args a) {
+__global__ __launch_bounds__(kThreads, (Occ<T, D>::value)) void colsum_kernel(P2Args a) {
   using G_ = Geo<T, D>;
   using MM = Mma<T>;
   using frag = typename MM::frag;
