@@ -609,39 +609,55 @@ __global__ __launch_bounds__(kThreads, (Occ<T, D>::value)) void rowstats_kernel(
 // Merge the chunk partials of every text row into lse = ln(sum exp(z)), and
 // (if lse2 is given) the same in log2 units for pass 2.  Pass 1 writes a
 // partial for every (chunk, row), empty (-inf, 0) where the row sees no key
-// of the chunk.
+// of the chunk.  Max and sum run over the chunks in ascending order.
+//
+// The loads of G chunks are issued together (a chunk index past nkc re-reads
+// the last chunk and is then ignored).  With at most G chunks, every partial
+// of the row is held in registers and read once: the kernel waits on one
+// round of loads; with more, the groups are read twice (max, then sum).
+template <int G>
 __global__ void lse_combine_kernel(const float *__restrict__ part_m, const float *__restrict__ part_l,
                                    int rows, int nkc, float *__restrict__ lse,
                                    float *__restrict__ lse2) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= rows) return;
-  // Chunks in groups of 8 whose loads are issued together (a chunk index past
-  // nkc re-reads the last chunk and is then ignored); max and sum run over
-  // the chunks in ascending order.
-  constexpr int kGroup = 8;
   auto at = [&](int c) __attribute__((always_inline)) {
     return (size_t)min(c, nkc - 1) * rows + idx;
   };
-  float M = -INFINITY;
-  for (int c0 = 0; c0 < nkc; c0 += kGroup) {
-    float m[kGroup];
+  float M = -INFINITY, S = 0.f;
+  if (nkc <= G) {
+    float m[G], l[G];
 #pragma unroll
-    for (int u = 0; u < kGroup; ++u) m[u] = part_m[at(c0 + u)];
-#pragma unroll
-    for (int u = 0; u < kGroup; ++u)
-      if (c0 + u < nkc) M = fmaxf(M, m[u]);
-  }
-  float S = 0.f;
-  for (int c0 = 0; c0 < nkc; c0 += kGroup) {
-    float m[kGroup], l[kGroup];
-#pragma unroll
-    for (int u = 0; u < kGroup; ++u) {
-      m[u] = part_m[at(c0 + u)];
-      l[u] = part_l[at(c0 + u)];
+    for (int u = 0; u < G; ++u) {
+      m[u] = part_m[at(u)];
+      l[u] = part_l[at(u)];
     }
 #pragma unroll
-    for (int u = 0; u < kGroup; ++u)
-      if (c0 + u < nkc && m[u] != -INFINITY) S += l[u] * __builtin_amdgcn_exp2f(m[u] - M);
+    for (int u = 0; u < G; ++u)
+      if (u < nkc) M = fmaxf(M, m[u]);
+#pragma unroll
+    for (int u = 0; u < G; ++u)
+      if (u < nkc && m[u] != -INFINITY) S += l[u] * __builtin_amdgcn_exp2f(m[u] - M);
+  } else {
+    for (int c0 = 0; c0 < nkc; c0 += G) {
+      float m[G];
+#pragma unroll
+      for (int u = 0; u < G; ++u) m[u] = part_m[at(c0 + u)];
+#pragma unroll
+      for (int u = 0; u < G; ++u)
+        if (c0 + u < nkc) M = fmaxf(M, m[u]);
+    }
+    for (int c0 = 0; c0 < nkc; c0 += G) {
+      float m[G], l[G];
+#pragma unroll
+      for (int u = 0; u < G; ++u) {
+        m[u] = part_m[at(c0 + u)];
+        l[u] = part_l[at(c0 + u)];
+      }
+#pragma unroll
+      for (int u = 0; u < G; ++u)
+        if (c0 + u < nkc && m[u] != -INFINITY) S += l[u] * __builtin_amdgcn_exp2f(m[u] - M);
+    }
   }
   const float v = (M + __builtin_amdgcn_logf(S)) * kLn2;
   lse[idx] = v;
@@ -992,8 +1008,16 @@ hipError_t run_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P, co
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int rows = Hq * L.T_tot;
-  hipLaunchKernelGGL(lse_combine_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, a.part_m,
-                     a.part_l, rows, P.nkc, row_lse, lse2);
+  const dim3 cg((rows + 255) / 256), cb(256);
+  if (P.nkc <= 8)
+    hipLaunchKernelGGL(lse_combine_kernel<8>, cg, cb, 0, st, a.part_m, a.part_l, rows, P.nkc,
+                       row_lse, lse2);
+  else if (P.nkc <= 16)
+    hipLaunchKernelGGL(lse_combine_kernel<16>, cg, cb, 0, st, a.part_m, a.part_l, rows, P.nkc,
+                       row_lse, lse2);
+  else
+    hipLaunchKernelGGL(lse_combine_kernel<32>, cg, cb, 0, st, a.part_m, a.part_l, rows, P.nkc,
+                       row_lse, lse2);
   return hipGetLastError();
 }
 
