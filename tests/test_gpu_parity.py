@@ -245,6 +245,35 @@ def test_budget_at_bounds(K_at):
     assert np.array_equal(g, O.budget(lay, S, 1.0, 50, 950, 4))
 
 
+@pytest.mark.parametrize("m", [16, 256])
+@pytest.mark.parametrize("mode", ["proportional", "raw"])
+def test_budget_at_the_size_limits(mode, m):
+    # up to AVTP_MAX_IMAGES_PER_SEQ images of up to AVTP_MAX_IMAGE_LEN tokens
+    # in one sequence (16: the one-wave rule; 256: token and keep totals near
+    # 2^28), with integer weights from 1 (an image with a vanishing share) to
+    # 2^28; the budget call reads no per-token data, so the layout costs
+    # nothing to build
+    rng = np.random.default_rng(31 + m)
+    n = [int(x) for x in rng.integers((1 << 20) - 4096, (1 << 20) + 1, size=m)]
+    n[0], n[1], n[2] = 1 << 20, 1, 0
+    S = (rng.lognormal(0.0, 3.0, size=m) * np.array(n, np.float64) / 100).astype(np.float32)
+    S[3], S[4] = np.float32(1e-30), np.float32(0.0)
+    bmode = O.BUDGET_RAW if mode == "raw" else O.BUDGET_PROPORTIONAL
+    lo = sum(O.budget_bounds(x, 50, 950, 16)[0] for x in n)
+    hi = sum(O.budget_bounds(x, 50, 950, 16)[1] for x in n)
+    for K in (lo, hi, (lo + hi) // 2, lo + 1, hi - 7):
+        lay = build_layout([n], 1, 2, 0)
+        lay.keep_total[:] = K
+        dl = A.DeviceLayout(lay)
+        say(f"[budget] {m} images, {sum(n)} tokens, K={K}, mode={mode}")
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+        g = A.budget(dl, torch.from_numpy(S).cuda(), 1.0, 50, 950, 16, bmode,
+                     status=status).cpu().numpy()
+        o = O.budget(lay, S, 1.0, 50, 950, 16, bmode)
+        assert np.array_equal(g, o), (K, mode)
+        assert int(g.sum()) == K and not status.any()
+
+
 # ------------------------------------------------------------------ select
 def _sel_layout(kind):
     if kind == "mixed":
