@@ -29,7 +29,10 @@ def test_abi_validation_is_clean_under_asan_and_ubsan(tmp_path):
     from paper_2608_26806_amd import build as B
     lib = B.build_host_sanitized(str(tmp_path / "libavtp_san.so"))
     env = dict(os.environ)
-    env.update(LD_PRELOAD=rt, AVTP_LIBRARY=lib,
+    # the ASan runtime must come first; anything the environment already
+    # preloads stays loaded after it
+    pre = env.get("LD_PRELOAD", "")
+    env.update(LD_PRELOAD=rt + (":" + pre if pre else ""), AVTP_LIBRARY=lib,
                ASAN_OPTIONS="detect_leaks=0:halt_on_error=1",
                UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
     r = subprocess.run([sys.executable, "-m", "pytest", os.path.join(ROOT, "tests", "test_abi.py"),
