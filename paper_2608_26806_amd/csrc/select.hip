@@ -87,19 +87,25 @@ enum BudMode {
   kBudWave = 2,    // the rule run by wave 0 while the other waves load the image
 };
 
-// exclusive block scan of a 0/1 flag (256 threads, 4 waves); returns the
-// exclusive count and writes the block total to *total
-__device__ inline int block_scan_flag(bool f, int *wsum, int *total) {
+// exclusive block scans of two 0/1 flags at once (256 threads, 4 waves):
+// returns the exclusive count of f, writes that of g to *g_before and the
+// block totals to *f_total and *g_total
+__device__ inline int block_scan_flags(bool f, bool g, int *wsum, int *f_total, int *g_before,
+                                       int *g_total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const unsigned long long m = __ballot(f);
-  const int below = __popcll(m & ((1ull << lane) - 1ull));
-  if (lane == 0) wsum[wave] = __popcll(m);
+  const unsigned long long mf = __ballot(f), mg = __ballot(g);
+  const unsigned long long below = (1ull << lane) - 1ull;
+  // per wave: the two counts packed in one int (each at most 64)
+  if (lane == 0) wsum[wave] = (__popcll(mg) << 16) | __popcll(mf);
   __syncthreads();
   int off = 0;
   for (int w = 0; w < wave; ++w) off += wsum[w];
-  *total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+  const int tot = wsum[0] + wsum[1] + wsum[2] + wsum[3];
   __syncthreads();
-  return off + below;
+  *f_total = tot & 0xffff;
+  *g_total = tot >> 16;
+  *g_before = (off >> 16) + __popcll(mg & below);
+  return (off & 0xffff) + __popcll(mf & below);
 }
 
 // exclusive block scan of an integer (256 threads); block total in *total
@@ -313,22 +319,25 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   }
   const uint32_t theta = prefix;  // exactly krem keys equal to theta are kept
 
-  // ---- ordered pass: keep > theta, and the first krem keys == theta
+  // ---- ordered pass: keep > theta, and the first krem keys == theta.  The
+  // kept keys before a key are the keys > theta before it plus the first
+  // krem of the keys == theta before it, so one scan of both counts places
+  // every kept key.
   if (in_lds) {
-    // each thread takes a contiguous run of keys; two block scans place them
+    // each thread takes a contiguous run of keys; the two counts share one
+    // 32-bit block scan (each is at most kLdsKeys < 2^16)
     const int per = (n + kThreads - 1) / kThreads;
     const int j0 = min(n, tid * per), j1 = min(n, j0 + per);
-    int ne = 0;
-    for (int j = j0; j < j1; ++j) ne += keys[j] == theta;
-    int tot;
-    int eq_rank = block_scan_int(ne, wsum, &tot);
-    int nk = 0;
-    for (int j = j0, r = eq_rank; j < j1; ++j) {
+    int ne = 0, ng = 0;
+    for (int j = j0; j < j1; ++j) {
       const uint32_t key = keys[j];
-      if (key > theta) ++nk;
-      else if (key == theta) nk += (r++ < krem);
+      ne += key == theta;
+      ng += key > theta;
     }
-    int pos = block_scan_int(nk, wsum, &tot);
+    int tot;
+    const int before = block_scan_int((ng << 16) | ne, wsum, &tot);
+    int eq_rank = before & 0xffff;
+    int pos = (before >> 16) + min(krem, eq_rank);
     for (int j = j0; j < j1; ++j) {
       const uint32_t key = keys[j];
       bool keep = key > theta;
@@ -337,19 +346,20 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
     }
     return;
   }
-  int eq_carry = 0, keep_carry = 0;
+  int eq_carry = 0, gt_carry = 0;
   for (int c0 = 0; c0 < n; c0 += kThreads) {
     const int j = c0 + tid;
     uint32_t key = 0;
     if (j < n) key = order_key(s[j]);
     const bool gt = j < n && key > theta;
     const bool eq = j < n && key == theta;
-    int tot;
-    const int eq_rank = block_scan_flag(eq, wsum, &tot) + eq_carry;
-    eq_carry += tot;
+    int eq_tot, gt_tot;
+    int gt_before;
+    const int eq_rank = block_scan_flags(eq, gt, wsum, &eq_tot, &gt_before, &gt_tot) + eq_carry;
     const bool keep = gt || (eq && eq_rank < krem);
-    const int pos = block_scan_flag(keep, wsum, &tot) + keep_carry;
-    keep_carry += tot;
+    const int pos = gt_carry + gt_before + min(krem, eq_rank);
+    eq_carry += eq_tot;
+    gt_carry += gt_tot;
     if (keep) put(base + pos, st + j, b);
   }
 }
