@@ -1,0 +1,101 @@
+"""Seeded random layouts through the attention score, against the oracle:
+every row LSE (within the dtype's tolerance, absolute), every visual score and
+every image sum (relative), both from the two-pass call and from pass 2 given
+the oracle's LSE, and the no-text-after flag exactly on the sequences where
+the oracle finds an image with no text row after it (its scores 0).
+
+The layouts put a random number of text rows before every image and after the
+last one (none included), with empty, one-token and ragged images and
+sequences without images; the head grouping, head size and dtype vary too.
+So the kernels' causal masks meet key tiles and stages that rows see in full,
+in part or not at all, rows of one block spread over the whole sequence, and
+pass 2's query split on most draws."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import TOL, assert_rel, need_gpu, say, to_dev
+from oracle import avtp_oracle as O
+from paper_2608_26806_amd import avtp as A
+from paper_2608_26806_amd.workloads import Layout, f32_to_bf16_bits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    need_gpu()
+    A.lib()
+
+
+def _random_layout(rng):
+    cu_seqlens, img_start, img_len, cu_img, text_pos, cu_text = [0], [], [], [0], [], [0]
+    pos = 0
+    for _ in range(int(rng.integers(1, 4))):
+        for _ in range(int(rng.choice([0, 1, 2, 4, 6]))):
+            nt = int(rng.integers(0, 6))
+            text_pos.extend(range(pos, pos + nt))
+            pos += nt
+            u = rng.random()
+            n = 0 if u < 0.05 else 1 if u < 0.1 else int(rng.integers(2, 600))
+            img_start.append(pos)
+            img_len.append(n)
+            pos += n
+        u = rng.random()
+        nt = 0 if u < 0.25 else int(rng.integers(200, 400)) if u < 0.35 else int(rng.integers(1, 41))
+        if pos == cu_seqlens[-1] and nt == 0:
+            nt = 1                                   # every sequence holds a token
+        text_pos.extend(range(pos, pos + nt))
+        pos += nt
+        cu_seqlens.append(pos)
+        cu_img.append(len(img_len))
+        cu_text.append(len(text_pos))
+    a = lambda v: np.asarray(v, dtype=np.int32)
+    return Layout(a(cu_seqlens), a(img_start), a(img_len), a(cu_img), a(text_pos), a(cu_text),
+                  np.zeros(len(cu_seqlens) - 1, np.int32))
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_layout_scores(seed):
+    rng = np.random.default_rng(2000 + seed)
+    lay = _random_layout(rng)
+    Hkv = int(rng.choice([1, 2]))
+    Hq = Hkv * int(rng.choice([1, 2, 4, 7]))
+    d = int(rng.choice([64, 128]))
+    dt = "fp32" if rng.random() < 0.25 else "bf16"
+    scale = d ** -0.5
+    q32 = rng.standard_normal((lay.T_tot, Hq, d)).astype(np.float32)
+    k32 = rng.standard_normal((lay.N_tok, Hkv, d)).astype(np.float32)
+    k32[lay.visual_mask()] *= np.float32(rng.uniform(0.5, 2.0))
+    q, k = (f32_to_bf16_bits(q32), f32_to_bf16_bits(k32)) if dt == "bf16" else (q32, k32)
+    say(f"[random scores] seed {seed}: B={lay.B} images={lay.n_img} N_tok={lay.N_tok} "
+        f"T={lay.T_tot} Hq={Hq} Hkv={Hkv} d={d} {dt}")
+    s_o, isum_o, lse_o, empty = O.attn_scores(lay, q, k, Hq, Hkv, scale, dt)
+
+    dl = A.DeviceLayout(lay)
+    qd, kd = to_dev(q, dt), to_dev(k, dt)
+    tol = TOL[dt]
+    vis = lay.visual_mask()
+    # which sequences hold an image with no text row after it
+    flagged = {int(np.searchsorted(lay.cu_img, i, side="right") - 1) for i in empty}
+
+    if lay.T_tot:
+        lse_g = A.row_lse(dl, qd, kd, scale).cpu().numpy().astype(np.float64)
+        assert_rel(lse_g, lse_o, 0.0, "row lse", abs_floor=tol)
+    lse_sup = torch.from_numpy(np.ascontiguousarray(lse_o, dtype=np.float32)).cuda()
+    for row_lse in (None, lse_sup):
+        status = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+        s_g, isum_g = A.score_attn(dl, qd, kd, scale, row_lse=row_lse, status=status)
+        s_g, isum_g = s_g.cpu().numpy(), isum_g.cpu().numpy()
+        what = "given lse" if row_lse is not None else "two passes"
+        assert_rel(s_g[vis], s_o[vis], tol, f"scores ({what})", abs_floor=1e-30)
+        assert np.all(np.isinf(s_g[~vis]) & (s_g[~vis] > 0))
+        if lay.n_img:
+            assert_rel(isum_g, isum_o, tol, f"image sums ({what})", abs_floor=1e-30)
+        st = status.cpu().numpy()
+        got = {b for b in range(lay.B) if st[b] & A.FLAG_NO_TEXT_AFTER}
+        assert got == flagged, (got, flagged)
+        assert not np.any(st & ~A.FLAG_NO_TEXT_AFTER)
+        for i in empty:
+            s0, n = int(lay.img_start[i]), int(lay.img_len[i])
+            assert np.all(s_g[s0:s0 + n] == 0.0)
