@@ -360,9 +360,10 @@ int avtp_select_compact(avtp_stream_t stream, const avtp_layout *layout, const f
   // bytes to move).  Every block of the fused kernel runs its image's
   // selection before it copies, so the copies cannot start before the
   // selections end; with more bytes to move the two kernels back to back are
-  // as fast or faster (measured with events around the calls: config 1,
-  // 0.4 MB: one launch 12.2 us, two 12.8; config 2, 15 MB: 17.0 and 16.2;
-  // config 3, 240 MB: 39 and 34), and are used instead.
+  // as fast or faster (measured with events around the calls: 0.4 MB moved
+  // (128 visual tokens): one launch 12.2 us, two 12.8; 15 MB (4 images of
+  // 729 tokens): 17.0 and 16.2; 240 MB (2 sequences of 8 images): 39 and
+  // 34), and are used instead.
   const int64_t moved = bytes_moved(need, tensors, n_tensors);
   hipStream_t st = (hipStream_t)stream;
   if (moved > kFusedMaxBytes) {
