@@ -11,6 +11,13 @@
 
 namespace avtp {
 
+// hipGetLastError() reports the last failed HIP call of the calling thread,
+// including calls the library's caller made before entering it.  Every
+// launch function reads it (which clears it) before its first launch, so
+// that the read after a launch reports that launch alone; an error of the
+// device itself (a broken context) still fails the launch and is reported.
+inline void clear_pending_error() { (void)hipGetLastError(); }
+
 // Device view of a validated layout (device pointers plus host-derived maxima).
 struct DevLayout {
   int B, n_img, N_tok, T_tot;

@@ -34,6 +34,7 @@ __global__ __launch_bounds__(NTH) void budget_kernel(const float *__restrict__ i
 hipError_t launch_budget(hipStream_t st, const DevLayout &L, const float *img_sum, int mode,
                          float alpha, int lo_permille, int hi_permille, int floor_abs,
                          int32_t *budget, int32_t *status) {
+  clear_pending_error();
   if (L.max_img_per_seq <= 16)
     hipLaunchKernelGGL(budget_kernel<64>, dim3(L.B), dim3(64), 0, st, img_sum, L.img_len, L.cu_img,
                        L.keep_total, mode, alpha, lo_permille, hi_permille, floor_abs, budget,

@@ -65,6 +65,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CArgs a) {
 
 hipError_t launch_compact(hipStream_t st, const DevLayout &L, const int32_t *keep_idx,
                           int64_t n_out, const avtp_tensor *tensors, int n_tensors) {
+  clear_pending_error();
   CArgs a;
   a.n = n_tensors;
   a.keep_idx = keep_idx;

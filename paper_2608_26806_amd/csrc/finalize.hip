@@ -101,6 +101,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
 
 hipError_t launch_finalize(hipStream_t st, const DevLayout &L, const float *colsum, int Hq,
                            int planes, float *scores, float *img_sum, int32_t *status) {
+  clear_pending_error();
   const int text_blocks = (L.T_tot + 255) / 256;
   const int grid = L.n_img + text_blocks;
   if (grid == 0) return hipSuccess;

@@ -90,6 +90,7 @@ __global__ __launch_bounds__(kSelThreads) void layer_select_kernel(const int32_t
 }  // namespace
 
 hipError_t launch_layer_attention(hipStream_t st, const DevLayout &L, const float *img_sum, float *A) {
+  clear_pending_error();
   if (L.B == 0) return hipSuccess;
   hipLaunchKernelGGL(layer_attn_kernel, dim3((L.B + 255) / 256), dim3(256), 0, st, img_sum, L.cu_img,
                      L.B, A);
@@ -98,6 +99,7 @@ hipError_t launch_layer_attention(hipStream_t st, const DevLayout &L, const floa
 
 hipError_t launch_layer_select(hipStream_t st, const float *A, int L, int N, int k, int32_t *rank_sum,
                                int32_t *selected) {
+  clear_pending_error();
   hipLaunchKernelGGL(layer_rank_kernel, dim3(L), dim3(kRankThreads), 0, st, A, L, N, rank_sum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -80,6 +80,7 @@ hipError_t launch_pruned_layout(hipStream_t st, const DevLayout &L, const int32_
                                 const int32_t *cu_out, int32_t *cu_seqlens_out,
                                 int32_t *img_start_out, int32_t *img_len_out, int32_t *cu_img_out,
                                 int32_t *text_pos_out, int32_t *cu_text_out) {
+  clear_pending_error();
   if (L.B == 0) return hipSuccess;
   hipLaunchKernelGGL(pruned_layout_kernel, dim3(L.B), dim3(kThreads), 0, st, L.img_start, L.img_len,
                      L.cu_img, L.text_pos, L.cu_text, keep_idx, cu_out, L.B, cu_seqlens_out,

@@ -1121,6 +1121,7 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
 hipError_t launch_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P, int dtype,
                           const void *q, const void *k, int Hq, int Hkv, int d, float scale,
                           float *row_lse, float *lse2, char *ws) {
+  clear_pending_error();
   if (dtype == AVTP_BF16)
     return d == 128 ? run_row_lse<__bf16, 128>(st, L, P, q, k, Hq, Hkv, scale, row_lse, lse2, ws)
                     : run_row_lse<__bf16, 64>(st, L, P, q, k, Hq, Hkv, scale, row_lse, lse2, ws);
@@ -1129,6 +1130,7 @@ hipError_t launch_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P,
 }
 
 hipError_t launch_lse_to_log2(hipStream_t st, int rows, const float *lse, float *lse2) {
+  clear_pending_error();
   if (rows <= 0) return hipSuccess;
   hipLaunchKernelGGL(lse_to_log2_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, lse, rows, lse2);
   return hipGetLastError();
@@ -1137,6 +1139,7 @@ hipError_t launch_lse_to_log2(hipStream_t st, int rows, const float *lse, float 
 hipError_t launch_colsum(hipStream_t st, const DevLayout &L, const AttnPlan &P, int dtype,
                          const void *q, const void *k, int Hq, int Hkv, int d, float scale,
                          const float *lse2, char *ws) {
+  clear_pending_error();
   if (dtype == AVTP_BF16)
     return d == 128 ? run_colsum<__bf16, 128>(st, L, P, q, k, Hq, Hkv, scale, lse2, ws)
                     : run_colsum<__bf16, 64>(st, L, P, q, k, Hq, Hkv, scale, lse2, ws);

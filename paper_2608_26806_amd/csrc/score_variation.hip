@@ -125,6 +125,7 @@ size_t variation_workspace_bytes(const DevLayout &) { return 0; }
 
 hipError_t launch_variation(hipStream_t st, const DevLayout &L, int dtype, const void *h_cur,
                             const void *h_prior, int hidden, float *scores) {
+  clear_pending_error();
   if (L.n_img == 0 || L.max_img_len == 0) return hipSuccess;
   const dim3 grid((L.max_img_len + kTokPerBlock - 1) / kTokPerBlock, L.n_img);
   if (dtype == AVTP_BF16)

@@ -495,6 +495,7 @@ hipError_t launch_select_compact(hipStream_t st, const DevLayout &L, const float
                                  const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
                                  int32_t *cu_out, int32_t *status, int64_t n_out,
                                  const avtp_tensor *tensors, int n_tensors) {
+  clear_pending_error();
   const SCArgs a = sc_args(L, scores, budget, keep_idx, keep_capacity, cu_out, status, n_out,
                            tensors, n_tensors);
   const int images = L.n_img > 0 ? L.n_img : 1;
@@ -506,6 +507,7 @@ hipError_t launch_select_compact(hipStream_t st, const DevLayout &L, const float
 hipError_t launch_select(hipStream_t st, const DevLayout &L, const float *scores,
                          const int32_t *budget, int32_t *keep_idx, int64_t keep_capacity,
                          int32_t *cu_out, int32_t *status) {
+  clear_pending_error();
   const int grid = L.n_img > 0 ? L.n_img : 1;
   const SelArgs A{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
                   L.B, L.n_img, L.T_tot, cu_out};
@@ -518,6 +520,7 @@ hipError_t launch_budget_select(hipStream_t st, const DevLayout &L, const float 
                                 float alpha, int lo_permille, int hi_permille, int floor_abs,
                                 const float *scores, int32_t *budget, int32_t *keep_idx,
                                 int64_t keep_capacity, int32_t *cu_out, int32_t *status) {
+  clear_pending_error();
   const int grid = L.n_img > 0 ? L.n_img : 1;
   const SelArgs A{scores, budget, L.img_start, L.img_len, L.cu_img, L.cu_text, L.text_pos,
                   L.B, L.n_img, L.T_tot, cu_out};
@@ -538,6 +541,7 @@ hipError_t launch_budget_select_compact(hipStream_t st, const DevLayout &L, cons
                                         int32_t *keep_idx, int64_t keep_capacity, int32_t *cu_out,
                                         int32_t *status, int64_t n_out, const avtp_tensor *tensors,
                                         int n_tensors) {
+  clear_pending_error();
   const SCArgs a = sc_args(L, scores, budget, keep_idx, keep_capacity, cu_out, status, n_out,
                            tensors, n_tensors);
   const int images = L.n_img > 0 ? L.n_img : 1;
