@@ -113,8 +113,34 @@ def _check(rc: int, where: str) -> None:
         raise AvtpError(rc, where)
 
 
-def _ptr(t: Optional[torch.Tensor]):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+def _arg(t: Optional[torch.Tensor], name: str, numel: int = 0, dtype=None):
+    """Device pointer of tensor argument ``name``, after the checks the C ABI
+    cannot make (it receives bare pointers): on the GPU, contiguous, of the
+    expected dtype and with at least ``numel`` elements, since a kernel would
+    otherwise read or write a host tensor or a short buffer out of bounds.
+    None passes through (optional arguments)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name}: a GPU tensor is needed, got one on {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: a contiguous tensor is needed")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name}: {dtype} is needed, got {t.dtype}")
+    if t.numel() < numel:
+        raise ValueError(f"{name}: at least {numel} elements are needed, got {t.numel()}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _check_qk(dl: "DeviceLayout", q_text: torch.Tensor, k: torch.Tensor) -> None:
+    """q_text [T_tot, Hq, d] and k [N_tok, Hkv, d] of one dtype."""
+    if q_text.dim() != 3 or k.dim() != 3 or q_text.shape[2] != k.shape[2]:
+        raise ValueError("q_text must be [T_tot, Hq, d] and k [N_tok, Hkv, d]")
+    if q_text.shape[0] != dl.T_tot or k.shape[0] != dl.N_tok:
+        raise ValueError(f"q_text has {q_text.shape[0]} rows and k {k.shape[0]}; the layout has "
+                         f"{dl.T_tot} text rows and {dl.N_tok} tokens")
+    if q_text.dtype != k.dtype:
+        raise TypeError(f"q_text ({q_text.dtype}) and k ({k.dtype}) differ in dtype")
 
 
 def _stream(stream=None):
@@ -198,8 +224,11 @@ def row_lse(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor, softmax_sca
         out = torch.empty((Hq, T), dtype=torch.float32, device=q_text.device)
     if ws is None:
         ws = alloc_workspace(score_workspace_bytes(dl, SCORE_ATTN, dt, Hq, Hkv, d), q_text.device)
-    _check(lib().avtp_row_lse(_stream(stream), dl.ref(), dt, _ptr(q_text), _ptr(k), Hq, Hkv, d,
-                              float(softmax_scale), _ptr(out), _ptr(ws), ws.numel()), "avtp_row_lse")
+    _check_qk(dl, q_text, k)
+    _check(lib().avtp_row_lse(_stream(stream), dl.ref(), dt, _arg(q_text, "q_text"),
+                              _arg(k, "k"), Hq, Hkv, d, float(softmax_scale),
+                              _arg(out, "out", Hq * dl.T_tot, torch.float32),
+                              _arg(ws, "ws", 0, torch.uint8), ws.numel()), "avtp_row_lse")
     return out
 
 
@@ -224,9 +253,13 @@ def prepare_score_attn(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor,
                        status: Optional[torch.Tensor] = None, stream=None) -> Prepared:
     """avtp_score (attention mode) on fixed buffers, as a Prepared call."""
     T, Hq, d = q_text.shape
-    args = (_stream(stream), dl.ref(), SCORE_ATTN, dtype_code(q_text), _ptr(q_text), _ptr(k), Hq,
-            k.shape[1], d, float(softmax_scale), _ptr(row_lse), None, None, 0, _ptr(scores),
-            _ptr(img_sum), _ptr(status), _ptr(ws), ws.numel())
+    _check_qk(dl, q_text, k)
+    args = (_stream(stream), dl.ref(), SCORE_ATTN, dtype_code(q_text), _arg(q_text, "q_text"),
+            _arg(k, "k"), Hq, k.shape[1], d, float(softmax_scale),
+            _arg(row_lse, "row_lse", Hq * dl.T_tot, torch.float32), None, None, 0,
+            _arg(scores, "scores", dl.N_tok, torch.float32),
+            _arg(img_sum, "img_sum", dl.n_img, torch.float32),
+            _arg(status, "status", dl.B, torch.int32), _arg(ws, "ws", 0, torch.uint8), ws.numel())
     return Prepared(lib().avtp_score, args, "avtp_score",
                     (dl, q_text, k, scores, img_sum, ws, row_lse, status, stream))
 
@@ -239,9 +272,14 @@ def prepare_budget_select_compact(dl: DeviceLayout, img_sum: torch.Tensor, score
                                   status: Optional[torch.Tensor] = None, stream=None) -> Prepared:
     """avtp_budget_select_compact on fixed buffers, as a Prepared call."""
     ts = _tensor_set(pairs)
-    args = (_stream(stream), dl.ref(), _ptr(img_sum), mode, float(alpha), lo_permille, hi_permille,
-            floor_abs, _ptr(scores), _ptr(budget_out), _ptr(keep_idx), keep_idx.numel(),
-            _ptr(cu_out), _ptr(status), ts.arr, ts.n)
+    _check_pairs(dl, ts, dl.N_out)
+    args = (_stream(stream), dl.ref(), _arg(img_sum, "img_sum", dl.n_img, torch.float32), mode,
+            float(alpha), lo_permille, hi_permille, floor_abs,
+            _arg(scores, "scores", dl.N_tok, torch.float32),
+            _arg(budget_out, "budget_out", dl.n_img, torch.int32),
+            _arg(keep_idx, "keep_idx", 0, torch.int32), keep_idx.numel(),
+            _arg(cu_out, "cu_out", dl.B + 1, torch.int32), _arg(status, "status", dl.B, torch.int32),
+            ts.arr, ts.n)
     return Prepared(lib().avtp_budget_select_compact, args, "avtp_budget_select_compact",
                     (dl, img_sum, scores, ts, budget_out, keep_idx, cu_out, status, stream))
 
@@ -260,9 +298,14 @@ def score_attn(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor, softmax_
         img_sum = torch.empty(max(1, dl.n_img), dtype=torch.float32, device=dev)
     if ws is None:
         ws = alloc_workspace(score_workspace_bytes(dl, SCORE_ATTN, dt, Hq, Hkv, d), dev)
-    _check(lib().avtp_score(_stream(stream), dl.ref(), SCORE_ATTN, dt, _ptr(q_text), _ptr(k), Hq,
-                            Hkv, d, float(softmax_scale), _ptr(row_lse), None, None, 0,
-                            _ptr(scores), _ptr(img_sum), _ptr(status), _ptr(ws), ws.numel()),
+    _check_qk(dl, q_text, k)
+    _check(lib().avtp_score(_stream(stream), dl.ref(), SCORE_ATTN, dt, _arg(q_text, "q_text"),
+                            _arg(k, "k"), Hq, Hkv, d, float(softmax_scale),
+                            _arg(row_lse, "row_lse", Hq * dl.T_tot, torch.float32), None, None, 0,
+                            _arg(scores, "scores", dl.N_tok, torch.float32),
+                            _arg(img_sum, "img_sum", dl.n_img, torch.float32),
+                            _arg(status, "status", dl.B, torch.int32),
+                            _arg(ws, "ws", 0, torch.uint8), ws.numel()),
            "avtp_score")
     return scores, img_sum[: dl.n_img]
 
@@ -275,10 +318,15 @@ def score_attn_noalloc(dl: DeviceLayout, q_text: torch.Tensor, k: torch.Tensor,
     library's own per-GPU scratch replaces the workspace."""
     T, Hq, d = q_text.shape
     Hkv = k.shape[1]
+    _check_qk(dl, q_text, k)
     _check(lib().avtp_score_noalloc(_stream(stream), dl.ref(), SCORE_ATTN, dtype_code(q_text),
-                                    _ptr(q_text), _ptr(k), Hq, Hkv, d, float(softmax_scale),
-                                    _ptr(row_lse), None, None, 0, _ptr(scores), _ptr(img_sum),
-                                    _ptr(status)), "avtp_score_noalloc")
+                                    _arg(q_text, "q_text"), _arg(k, "k"), Hq, Hkv, d,
+                                    float(softmax_scale),
+                                    _arg(row_lse, "row_lse", Hq * dl.T_tot, torch.float32), None,
+                                    None, 0, _arg(scores, "scores", dl.N_tok, torch.float32),
+                                    _arg(img_sum, "img_sum", dl.n_img, torch.float32),
+                                    _arg(status, "status", dl.B, torch.int32)),
+           "avtp_score_noalloc")
     return scores, img_sum[: dl.n_img]
 
 
@@ -292,9 +340,15 @@ def score_variation(dl: DeviceLayout, h_cur: torch.Tensor, h_prior: torch.Tensor
     if img_sum is None:
         img_sum = torch.empty(max(1, dl.n_img), dtype=torch.float32, device=dev)
     ws = alloc_workspace(score_workspace_bytes(dl, SCORE_VARIATION), dev)
+    if h_cur.shape != h_prior.shape or h_cur.dtype != h_prior.dtype or h_cur.shape[0] != dl.N_tok:
+        raise ValueError("h_cur and h_prior must both be [N_tok, hidden] of one dtype")
     _check(lib().avtp_score(_stream(stream), dl.ref(), SCORE_VARIATION, dtype_code(h_cur), None,
-                            None, 0, 0, 0, 1.0, None, _ptr(h_cur), _ptr(h_prior), hidden,
-                            _ptr(scores), _ptr(img_sum), _ptr(status), _ptr(ws), ws.numel()),
+                            None, 0, 0, 0, 1.0, None, _arg(h_cur, "h_cur"),
+                            _arg(h_prior, "h_prior"), hidden,
+                            _arg(scores, "scores", dl.N_tok, torch.float32),
+                            _arg(img_sum, "img_sum", dl.n_img, torch.float32),
+                            _arg(status, "status", dl.B, torch.int32),
+                            _arg(ws, "ws", 0, torch.uint8), ws.numel()),
            "avtp_score")
     return scores, img_sum[: dl.n_img]
 
@@ -306,8 +360,11 @@ def budget(dl: DeviceLayout, img_sum: torch.Tensor, alpha: float = 1.0, lo_permi
            stream=None) -> torch.Tensor:
     if out is None:
         out = torch.empty(max(1, dl.n_img), dtype=torch.int32, device=img_sum.device)
-    _check(lib().avtp_budget(_stream(stream), dl.ref(), _ptr(img_sum), mode, float(alpha),
-                             lo_permille, hi_permille, floor_abs, _ptr(out), _ptr(status)),
+    _check(lib().avtp_budget(_stream(stream), dl.ref(),
+                             _arg(img_sum, "img_sum", dl.n_img, torch.float32), mode, float(alpha),
+                             lo_permille, hi_permille, floor_abs,
+                             _arg(out, "out", dl.n_img, torch.int32),
+                             _arg(status, "status", dl.B, torch.int32)),
            "avtp_budget")
     return out[: dl.n_img]
 
@@ -321,8 +378,12 @@ def select(dl: DeviceLayout, scores: torch.Tensor, budget_: torch.Tensor,
         keep_idx = torch.empty(max(1, dl.N_out), dtype=torch.int32, device=dev)
     if cu_out is None:
         cu_out = torch.empty(dl.B + 1, dtype=torch.int32, device=dev)
-    _check(lib().avtp_select(_stream(stream), dl.ref(), _ptr(scores), _ptr(budget_),
-                             _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out), _ptr(status)),
+    _check(lib().avtp_select(_stream(stream), dl.ref(),
+                             _arg(scores, "scores", dl.N_tok, torch.float32),
+                             _arg(budget_, "budget", dl.n_img, torch.int32),
+                             _arg(keep_idx, "keep_idx", 0, torch.int32), keep_idx.numel(),
+                             _arg(cu_out, "cu_out", dl.B + 1, torch.int32),
+                             _arg(status, "status", dl.B, torch.int32)),
            "avtp_select")
     return keep_idx[: dl.N_out], cu_out
 
@@ -362,13 +423,32 @@ def _tensor_set(pairs) -> TensorSet:
     return pairs if isinstance(pairs, TensorSet) else TensorSet(pairs)
 
 
+def _check_pairs(dl: DeviceLayout, ts: TensorSet, n_out: int) -> None:
+    """Every compaction pair on the GPU, source and destination of one dtype
+    and row shape, with at least N_tok source rows and n_out destination rows
+    along the token dimension (the kernels write every row below n_out)."""
+    for p in ts.pairs:
+        src, dst, td = p[0], p[1], (p[2] if len(p) > 2 else 0)
+        if not (src.is_cuda and dst.is_cuda):
+            raise ValueError("compaction tensors must be on the GPU")
+        if src.dtype != dst.dtype:
+            raise TypeError(f"compaction source ({src.dtype}) and destination ({dst.dtype}) differ")
+        if src.shape[:td] + src.shape[td + 1:] != dst.shape[:td] + dst.shape[td + 1:]:
+            raise ValueError(f"compaction rows differ: {tuple(src.shape)} -> {tuple(dst.shape)}")
+        if src.shape[td] < dl.N_tok or dst.shape[td] < n_out:
+            raise ValueError(f"compaction needs {dl.N_tok} source and {n_out} destination rows, "
+                             f"got {src.shape[td]} and {dst.shape[td]}")
+
+
 def compact(dl: DeviceLayout, keep_idx: torch.Tensor, pairs, n_out: Optional[int] = None,
             stream=None) -> None:
     """pairs: (src, dst) or (src, dst, token_dim) tuples, or a TensorSet of
     them; dst is written in place."""
     ts = _tensor_set(pairs)
     n = dl.N_out if n_out is None else int(n_out)
-    _check(lib().avtp_compact(_stream(stream), dl.ref(), _ptr(keep_idx), n, ts.arr, ts.n),
+    _check_pairs(dl, ts, n)
+    _check(lib().avtp_compact(_stream(stream), dl.ref(), _arg(keep_idx, "keep_idx", n, torch.int32),
+                              n, ts.arr, ts.n),
            "avtp_compact")
 
 
@@ -382,8 +462,13 @@ def select_compact(dl: DeviceLayout, scores: torch.Tensor, budget_: torch.Tensor
     if cu_out is None:
         cu_out = torch.empty(dl.B + 1, dtype=torch.int32, device=dev)
     ts = _tensor_set(pairs)
-    _check(lib().avtp_select_compact(_stream(stream), dl.ref(), _ptr(scores), _ptr(budget_),
-                                     _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out), _ptr(status),
+    _check_pairs(dl, ts, dl.N_out)
+    _check(lib().avtp_select_compact(_stream(stream), dl.ref(),
+                                     _arg(scores, "scores", dl.N_tok, torch.float32),
+                                     _arg(budget_, "budget", dl.n_img, torch.int32),
+                                     _arg(keep_idx, "keep_idx", 0, torch.int32), keep_idx.numel(),
+                                     _arg(cu_out, "cu_out", dl.B + 1, torch.int32),
+                                     _arg(status, "status", dl.B, torch.int32),
                                      ts.arr, ts.n), "avtp_select_compact")
     return keep_idx[: dl.N_out], cu_out
 
@@ -405,10 +490,15 @@ def budget_select_compact(dl: DeviceLayout, img_sum: torch.Tensor, scores: torch
     if cu_out is None:
         cu_out = torch.empty(dl.B + 1, dtype=torch.int32, device=dev)
     ts = _tensor_set(pairs)
+    _check_pairs(dl, ts, dl.N_out)
     _check(lib().avtp_budget_select_compact(
-        _stream(stream), dl.ref(), _ptr(img_sum), mode, float(alpha), lo_permille, hi_permille,
-        floor_abs, _ptr(scores), _ptr(budget_out), _ptr(keep_idx), keep_idx.numel(), _ptr(cu_out),
-        _ptr(status), ts.arr, ts.n), "avtp_budget_select_compact")
+        _stream(stream), dl.ref(), _arg(img_sum, "img_sum", dl.n_img, torch.float32), mode,
+        float(alpha), lo_permille, hi_permille, floor_abs,
+        _arg(scores, "scores", dl.N_tok, torch.float32),
+        _arg(budget_out, "budget_out", dl.n_img, torch.int32),
+        _arg(keep_idx, "keep_idx", 0, torch.int32), keep_idx.numel(),
+        _arg(cu_out, "cu_out", dl.B + 1, torch.int32), _arg(status, "status", dl.B, torch.int32),
+        ts.arr, ts.n), "avtp_budget_select_compact")
     return budget_out[: dl.n_img], keep_idx[: dl.N_out], cu_out
 
 
@@ -437,12 +527,16 @@ def pruned_layout(dl: DeviceLayout, keep_idx: torch.Tensor, cu_out: torch.Tensor
                for n, m in (("cu_seqlens", dl.B + 1), ("img_start", dl.n_img),
                             ("img_len", dl.n_img), ("cu_img", dl.B + 1), ("text_pos", dl.T_tot),
                             ("cu_text", dl.B + 1))}
-    _check(lib().avtp_pruned_layout(_stream(stream), dl.ref(), _ptr(keep_idx), _ptr(cu_out),
-                                    *[_ptr(out[n]) for n in ("cu_seqlens", "img_start", "img_len",
-                                                             "cu_img", "text_pos", "cu_text")]),
-           "avtp_pruned_layout")
     lens = {"cu_seqlens": dl.B + 1, "img_start": dl.n_img, "img_len": dl.n_img,
             "cu_img": dl.B + 1, "text_pos": dl.T_tot, "cu_text": dl.B + 1}
+    _check(lib().avtp_pruned_layout(_stream(stream), dl.ref(),
+                                    # (its length is cu_out[B], a device value)
+                                    _arg(keep_idx, "keep_idx", 0, torch.int32),
+                                    _arg(cu_out, "cu_out", dl.B + 1, torch.int32),
+                                    *[_arg(out[n], n, lens[n], torch.int32)
+                                      for n in ("cu_seqlens", "img_start", "img_len", "cu_img",
+                                                "text_pos", "cu_text")]),
+           "avtp_pruned_layout")
     return {n: t[: lens[n]] for n, t in out.items()}
 
 
@@ -452,7 +546,9 @@ def layer_attention(dl: DeviceLayout, img_sum: torch.Tensor, out: Optional[torch
     """A [B] fp32: per sequence (sample), the sum of its image sums (one layer)."""
     if out is None:
         out = torch.empty(max(1, dl.B), dtype=torch.float32, device=img_sum.device)
-    _check(lib().avtp_layer_attention(_stream(stream), dl.ref(), _ptr(img_sum), _ptr(out)),
+    _check(lib().avtp_layer_attention(_stream(stream), dl.ref(),
+                                      _arg(img_sum, "img_sum", dl.n_img, torch.float32),
+                                      _arg(out, "out", dl.B, torch.float32)),
            "avtp_layer_attention")
     return out[: dl.B]
 
@@ -468,6 +564,8 @@ def layer_select(A: torch.Tensor, k: int, rank_sum: Optional[torch.Tensor] = Non
         rank_sum = torch.empty(max(1, L), dtype=torch.int32, device=A.device)
     if selected is None:
         selected = torch.empty(max(1, k), dtype=torch.int32, device=A.device)
-    _check(lib().avtp_layer_select(_stream(stream), _ptr(A), L, N, int(k), _ptr(rank_sum),
-                                   _ptr(selected)), "avtp_layer_select")
+    _check(lib().avtp_layer_select(_stream(stream), _arg(A, "A", L * N, torch.float32), L, N,
+                                   int(k), _arg(rank_sum, "rank_sum", L, torch.int32),
+                                   _arg(selected, "selected", max(0, int(k)), torch.int32)),
+           "avtp_layer_select")
     return rank_sum[:L], selected[:k]

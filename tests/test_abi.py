@@ -258,3 +258,27 @@ def test_noalloc_rejects_oversize_and_bad_args_on_the_host():
     rc = lib.avtp_score_noalloc(None, small.ref(), A.SCORE_ATTN, A.BF16, p, p, 4, 2, 128, 0.1,
                                 None, None, None, 0, None, p, None)
     assert rc == A.ERR_INVALID_ARG
+
+
+def test_binding_rejects_host_tensors_and_mismatched_shapes():
+    # the binding checks what the C ABI cannot see in a bare pointer, before
+    # calling it: a host tensor handed to a kernel would be read as device
+    # memory (a raw stream handle keeps torch's GPU state out of this test)
+    dl = _dl()
+    raw = ctypes.c_void_p(0)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        A.budget(dl, torch.zeros(dl.n_img), 1.0, stream=raw)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        A.select(dl, torch.zeros(dl.N_tok), torch.zeros(dl.n_img, dtype=torch.int32), stream=raw)
+    q = torch.zeros(dl.T_tot + 1, 4, 128, dtype=torch.bfloat16)     # one text row too many
+    k = torch.zeros(dl.N_tok, 2, 128, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="text rows"):
+        A.score_attn(dl, q, k, 0.1, scores=torch.zeros(dl.N_tok), img_sum=torch.zeros(dl.n_img),
+                     ws=torch.zeros(1, dtype=torch.uint8), stream=raw)
+    with pytest.raises(TypeError, match="dtype"):
+        A.row_lse(dl, q[:dl.T_tot], k.float(), 0.1, out=torch.zeros(4, dl.T_tot),
+                  ws=torch.zeros(1, dtype=torch.uint8), stream=raw)
+    src = torch.zeros(dl.N_tok, 8)
+    with pytest.raises(ValueError, match="on the GPU"):
+        A.compact(dl, torch.zeros(dl.N_out, dtype=torch.int32), [(src, torch.zeros(dl.N_out, 8))],
+                  stream=raw)

@@ -57,3 +57,32 @@ def test_calls_after_a_failed_caller_hip_call_succeed():
     g = bud.cpu().numpy()
     assert np.array_equal(g, O.budget(lay, isum.cpu().numpy(), wl.alpha, wl.lo_permille,
                                       wl.hi_permille, wl.floor_abs))
+
+
+def test_binding_rejects_short_buffers_wrong_dtypes_and_small_destinations():
+    # checked in the binding before the call: a kernel would otherwise read or
+    # write past the end of a short buffer
+    wl = make_workload(2)
+    dl = A.DeviceLayout(wl.layout)
+    isum = torch.rand(dl.n_img, device="cuda")
+    scores = torch.rand(dl.N_tok, device="cuda")
+    bud = A.budget(dl, isum, 1.0)
+    say("[errors] binding argument checks")
+    with pytest.raises(ValueError, match="at least"):
+        A.select(dl, scores[: dl.N_tok - 1], bud)
+    with pytest.raises(TypeError, match="float32"):
+        A.budget(dl, isum.double(), 1.0)
+    with pytest.raises(ValueError, match="contiguous"):
+        A.select(dl, torch.rand(dl.N_tok, 2, device="cuda")[:, 0], bud)
+    keep, _ = A.select(dl, scores, bud)
+    src = torch.rand(dl.N_tok, 16, device="cuda")
+    with pytest.raises(ValueError, match="destination rows"):
+        A.compact(dl, keep, [(src, torch.empty(dl.N_out - 1, 16, device="cuda"))])
+    with pytest.raises(TypeError, match="differ"):
+        A.compact(dl, keep, [(src, torch.empty(dl.N_out, 16, device="cuda", dtype=torch.float16))])
+    with pytest.raises(ValueError, match="rows differ"):
+        A.compact(dl, keep, [(src, torch.empty(dl.N_out, 8, device="cuda"))])
+    out = torch.empty(dl.N_out, 16, device="cuda")
+    A.compact(dl, keep, [(src, out)])                   # the well-formed call still runs
+    torch.cuda.synchronize()
+    assert torch.equal(out, src[keep.long()])
