@@ -134,28 +134,36 @@ __device__ inline long long block_sum_ll(long long v, long long *sh) {
 constexpr int kLdsKeys = 4096;  // images up to this length keep their keys in LDS
 
 // Digit of the krem-th largest key among those matching (prefix, mask), from
-// a 256-bin histogram of byte `shift`; updates krem to the rank inside the bin.
-__device__ inline void pick_digit(const uint32_t *hist, int krem, uint32_t *sh_digit, int *sh_krem) {
-  if (threadIdx.x < 64) {
-    // lane l owns bins 4*o .. 4*o+3 with o = 63 - l, so that a prefix sum
-    // over the lanes is the sum over the bins from the highest down to its own
-    const int o = 63 - (int)threadIdx.x;
-    const int c = hist[4 * o] + hist[4 * o + 1] + hist[4 * o + 2] + hist[4 * o + 3];
-    const int suf = (int)wave::prefix_sum((uint32_t)c);
-    const int above = suf - c;  // keys in higher bins
-    const int lane = o;
-    if (suf >= krem && above < krem) {
-      int acc = above;
-      for (int x = 4 * lane + 3; x >= 4 * lane; --x) {
-        if (acc + (int)hist[x] >= krem) {
-          *sh_digit = (uint32_t)x;
-          *sh_krem = krem - acc;
-          break;
-        }
-        acc += hist[x];
-      }
+// a 256-bin histogram of one byte (16-byte aligned); krem becomes the rank
+// inside that bin.  Every wave calls it and gets the same, wave-uniform
+// result, so no wave waits for another to publish it.
+__device__ inline void pick_digit(const uint32_t *hist, int &krem, uint32_t &digit) {
+  // lane l owns bins 4*o .. 4*o+3 with o = 63 - l, so that a prefix sum over
+  // the lanes is the sum over the bins from the highest down to its own
+  const int o = 63 - (int)(threadIdx.x & 63);
+  const uint4 b = *reinterpret_cast<const uint4 *>(hist + 4 * o);
+  const int c = (int)(b.x + b.y + b.z + b.w);
+  const int suf = (int)wave::prefix_sum((uint32_t)c);
+  const int above = suf - c;  // keys in higher bins
+  // exactly one lane holds the krem-th key (1 <= krem <= the keys counted)
+  const bool mine = suf >= krem && above < krem;
+  const int src = __builtin_ctzll(__ballot(mine));
+  // that lane: its bins from the highest down
+  int d = 4 * o, r = krem - above;
+  if (r > (int)b.w) {
+    r -= (int)b.w;
+    if (r > (int)b.z) {
+      r -= (int)b.z;
+      if (r > (int)b.y) r -= (int)b.y;
+      else d += 1;
+    } else {
+      d += 2;
     }
+  } else {
+    d += 3;
   }
+  digit = (uint32_t)__builtin_amdgcn_readlane(d, src);
+  krem = __builtin_amdgcn_readlane(r, src);
 }
 
 // One block per image.  Besides the image's kept tokens, the block writes
@@ -179,12 +187,11 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
                                                                    const RuleArgs &R, int i,
                                                                    bool write, int32_t *status,
                                                                    Put put) {
-  __shared__ uint32_t hist[2][256];  // double-buffered across the radix passes
+  __shared__ __attribute__((aligned(16))) uint32_t hist[3][256];  // one per pass, used in turn
   __shared__ uint32_t keys[kLdsKeys];
   __shared__ int wsum[4];
   __shared__ long long red[4];
-  __shared__ uint32_t sh_digit[4];  // one slot per radix pass
-  __shared__ int sh_krem[4], sh_b, cnt[2];
+  __shared__ int sh_b, cnt[2];
   __shared__ int32_t bud_sh[AVTP_MAX_IMAGES_PER_SEQ];  // the in-block budgets of b's images
   const int tid = threadIdx.x;
   const float *__restrict__ scores = A.scores;
@@ -223,7 +230,7 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
     if (in_lds)
 #pragma unroll 4
       for (int j = u; j < n; j += nt) keys[j] = order_key(scores[st + j]);
-    for (int x = u; x < 256; x += nt) hist[0][x] = 0;
+    for (int x = u; x < 256; x += nt) hist[0][x] = hist[1][x] = 0;
     const int pend = first ? 0 : img_start[i - 1] + img_len[i - 1];
     int before = 0, between = 0;
     for (int t = a_lo + u; t < a_hi; t += nt) {
@@ -299,23 +306,24 @@ __device__ __attribute__((always_inline)) inline void select_image(const SelArgs
   // ---- radix select of the k-th largest key
   uint32_t prefix = 0, mask = 0;
   int krem = k;
-  // Two barriers per pass: pass p counts into hist[p & 1] (cleared during
-  // pass p - 1, or above for p = 0) while the other buffer, last read by
-  // pass p - 1's digit pick, is cleared for pass p + 1.
+  // One barrier per pass: pass p counts into hist[p % 3], which was cleared
+  // above (p < 2) or after the barrier of pass p - 2; after its own barrier
+  // every wave reads the complete histogram and picks the digit itself, and
+  // the block clears hist[(p + 2) % 3], which pass p - 1's picks read before
+  // every wave reached this barrier.
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    uint32_t *h = hist[pass & 1];
+    uint32_t *h = hist[pass % 3];
     for (int j = tid; j < n; j += kThreads) {
       const uint32_t key = in_lds ? keys[j] : order_key(s[j]);
       if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
     }
     __syncthreads();  // the histogram is complete
-    pick_digit(h, krem, &sh_digit[pass], &sh_krem[pass]);
-    hist[(pass + 1) & 1][tid] = 0;
-    __syncthreads();  // the digit is published and the next buffer is clear
-    prefix |= sh_digit[pass] << shift;
+    if (pass + 2 < 4) hist[(pass + 2) % 3][tid] = 0;
+    uint32_t digit;
+    pick_digit(h, krem, digit);
+    prefix |= digit << shift;
     mask |= 255u << shift;
-    krem = sh_krem[pass];
   }
   const uint32_t theta = prefix;  // exactly krem keys equal to theta are kept
 
