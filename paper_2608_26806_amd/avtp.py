@@ -133,10 +133,11 @@ def _arg(t: Optional[torch.Tensor], name: str, numel: int = 0, dtype=None):
 
 
 def _check_qk(dl: "DeviceLayout", q_text: torch.Tensor, k: torch.Tensor) -> None:
-    """q_text [T_tot, Hq, d] and k [N_tok, Hkv, d] of one dtype."""
+    """q_text [T_tot, Hq, d] and k [N_tok, Hkv, d] of one dtype (more rows are
+    allowed: the kernels read rows below T_tot and N_tok only)."""
     if q_text.dim() != 3 or k.dim() != 3 or q_text.shape[2] != k.shape[2]:
         raise ValueError("q_text must be [T_tot, Hq, d] and k [N_tok, Hkv, d]")
-    if q_text.shape[0] != dl.T_tot or k.shape[0] != dl.N_tok:
+    if q_text.shape[0] < dl.T_tot or k.shape[0] < dl.N_tok:
         raise ValueError(f"q_text has {q_text.shape[0]} rows and k {k.shape[0]}; the layout has "
                          f"{dl.T_tot} text rows and {dl.N_tok} tokens")
     if q_text.dtype != k.dtype:

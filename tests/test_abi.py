@@ -270,13 +270,14 @@ def test_binding_rejects_host_tensors_and_mismatched_shapes():
         A.budget(dl, torch.zeros(dl.n_img), 1.0, stream=raw)
     with pytest.raises(ValueError, match="GPU tensor"):
         A.select(dl, torch.zeros(dl.N_tok), torch.zeros(dl.n_img, dtype=torch.int32), stream=raw)
-    q = torch.zeros(dl.T_tot + 1, 4, 128, dtype=torch.bfloat16)     # one text row too many
+    q = torch.zeros(dl.T_tot - 1, 4, 128, dtype=torch.bfloat16)     # one text row too few
     k = torch.zeros(dl.N_tok, 2, 128, dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="text rows"):
         A.score_attn(dl, q, k, 0.1, scores=torch.zeros(dl.N_tok), img_sum=torch.zeros(dl.n_img),
                      ws=torch.zeros(1, dtype=torch.uint8), stream=raw)
     with pytest.raises(TypeError, match="dtype"):
-        A.row_lse(dl, q[:dl.T_tot], k.float(), 0.1, out=torch.zeros(4, dl.T_tot),
+        A.row_lse(dl, torch.zeros(dl.T_tot, 4, 128, dtype=torch.bfloat16), k.float(), 0.1,
+                  out=torch.zeros(4, dl.T_tot),
                   ws=torch.zeros(1, dtype=torch.uint8), stream=raw)
     src = torch.zeros(dl.N_tok, 8)
     with pytest.raises(ValueError, match="on the GPU"):
