@@ -129,7 +129,8 @@ typedef struct {
  * accumulation; the attention matrix is never stored.  If row_lse is given
  * (e.g. the softmax LSE of the layer's own fused attention, natural log,
  * [Hq, T_tot] fp32) the first pass is skipped.
- *   q_text [T_tot, Hq, d]  queries of the text rows (dtype)
+ *   q_text [T_tot, Hq, d]  queries of the text rows (dtype; may be NULL when
+ *                          T_tot = 0: every image then has no text row after it)
  *   k      [N_tok, Hkv, d] the layer's keys (dtype)
  *   d in {64, 128}, Hq % Hkv == 0.
  *
@@ -154,7 +155,8 @@ int avtp_score(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
 
 /* The first pass of AVTP_SCORE_ATTN alone: row_lse_out [Hq, T_tot] fp32,
  * natural-log LSE of each text row's causal attention logits (definition
- * above).  Same arguments and workspace as avtp_score. */
+ * above).  Same arguments and workspace as avtp_score; q_text and
+ * row_lse_out may be NULL when T_tot = 0 (nothing is launched). */
 int avtp_row_lse(avtp_stream_t stream, const avtp_layout *layout, int dtype, const void *q_text,
                  const void *k, int Hq, int Hkv, int d, float softmax_scale, float *row_lse_out,
                  void *ws, size_t ws_bytes);

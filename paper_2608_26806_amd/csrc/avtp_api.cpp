@@ -141,7 +141,10 @@ int avtp_row_lse(avtp_stream_t stream, const avtp_layout *layout, int dtype, con
   if (rc != AVTP_OK) return rc;
   if ((rc = check_attn_args(dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
   if ((rc = check_attn_extent(L, dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
-  if (!q_text || !k || !row_lse_out || !(std::isfinite(softmax_scale)) || softmax_scale <= 0.f)
+  // without text rows there is nothing to read or write through q_text and
+  // row_lse_out (an empty buffer may have no address)
+  if ((L.T_tot > 0 && (!q_text || !row_lse_out)) || !k || !(std::isfinite(softmax_scale)) ||
+      softmax_scale <= 0.f)
     return AVTP_ERR_INVALID_ARG;
   if ((uintptr_t)q_text % 16 || (uintptr_t)k % 16) return AVTP_ERR_INVALID_ARG;
   AttnPlan P = attn_plan(L, Hq, Hkv, d, dtype);
@@ -182,7 +185,8 @@ int score_impl(avtp_stream_t stream, const avtp_layout *layout, int mode, int dt
   if (mode != AVTP_SCORE_ATTN) return AVTP_ERR_INVALID_ARG;
   if ((rc = check_attn_args(dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
   if ((rc = check_attn_extent(L, dtype, Hq, Hkv, d)) != AVTP_OK) return rc;
-  if (!q_text || !k || !(std::isfinite(softmax_scale)) || softmax_scale <= 0.f)
+  // without text rows no query is read (an empty buffer may have no address)
+  if ((L.T_tot > 0 && !q_text) || !k || !(std::isfinite(softmax_scale)) || softmax_scale <= 0.f)
     return AVTP_ERR_INVALID_ARG;
   if ((uintptr_t)q_text % 16 || (uintptr_t)k % 16 || (row_lse && (uintptr_t)row_lse % 4))
     return AVTP_ERR_INVALID_ARG;

@@ -283,3 +283,20 @@ def test_binding_rejects_host_tensors_and_mismatched_shapes():
     with pytest.raises(ValueError, match="on the GPU"):
         A.compact(dl, torch.zeros(dl.N_out, dtype=torch.int32), [(src, torch.zeros(dl.N_out, 8))],
                   stream=raw)
+
+
+def test_row_lse_without_text_rows_needs_no_query_pointer():
+    # a batch with no text rows: nothing is read or written through q_text and
+    # row_lse_out (an empty tensor may have no address), and nothing is launched
+    lay = build_layout([[6, 4], [5]], 0, 0, 50)
+    assert lay.T_tot == 0
+    dl = _dl(lay)
+    buf = torch.zeros(1 << 16, dtype=torch.uint8)
+    ws = ctypes.c_void_p((buf.data_ptr() + 255) // 256 * 256)
+    k = ctypes.c_void_p(ws.value)
+    rc = A.lib().avtp_row_lse(None, dl.ref(), A.BF16, None, k, 4, 2, 128, 0.1, None, ws,
+                              buf.numel() - 256)
+    assert rc == A.OK
+    # with text rows the same null pointers are rejected
+    assert A.lib().avtp_row_lse(None, _dl().ref(), A.BF16, None, k, 4, 2, 128, 0.1, None, ws,
+                                buf.numel() - 256) == A.ERR_INVALID_ARG

@@ -99,3 +99,27 @@ def test_random_layout_scores(seed):
         for i in empty:
             s0, n = int(lay.img_start[i]), int(lay.img_len[i])
             assert np.all(s_g[s0:s0 + n] == 0.0)
+
+
+def test_batch_without_text_rows():
+    # no text row anywhere: no query to read, every visual score 0 and every
+    # sequence with a non-empty image flagged
+    from paper_2608_26806_amd.workloads import build_layout
+    lay = build_layout([[6, 0, 40], [], [300]], 0, 0, 50)   # the middle sequence is empty
+    assert lay.T_tot == 0
+    dl = A.DeviceLayout(lay)
+    k = torch.randn(lay.N_tok, 2, 128, device="cuda").to(torch.bfloat16)
+    q = torch.empty(0, 4, 128, device="cuda", dtype=torch.bfloat16)
+    status = torch.zeros(lay.B, dtype=torch.int32, device="cuda")
+    s_g, isum_g = A.score_attn(dl, q, k, 128 ** -0.5, status=status)
+    assert A.row_lse(dl, q, k, 128 ** -0.5).numel() == 0
+    torch.cuda.synchronize()
+    s_g = s_g.cpu().numpy()
+    vis = lay.visual_mask()
+    assert np.all(s_g[vis] == 0.0) and np.all(np.isinf(s_g[~vis]))
+    assert np.all(isum_g.cpu().numpy() == 0.0)
+    s_o, isum_o, _, empty = O.attn_scores(lay, np.zeros((0, 4, 128), np.uint16),
+                                          np.zeros((lay.N_tok, 2, 128), np.uint16), 4, 2,
+                                          128 ** -0.5, "bf16")
+    assert np.all(s_o[vis] == 0.0) and empty == {0, 2, 3}
+    assert [int(x) for x in status.cpu().numpy()] == [A.FLAG_NO_TEXT_AFTER, 0, A.FLAG_NO_TEXT_AFTER]
