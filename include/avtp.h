@@ -89,7 +89,9 @@ typedef enum {
  * keep_total[b] is the number of visual tokens sequence b keeps.
  * Each int32 array is given twice: as device memory (read by the kernels)
  * and as a host mirror with identical contents (read by the host-side
- * validation and launch sizing; never dereferenced on the device).
+ * validation and launch sizing; never dereferenced on the device).  Arrays
+ * of length 0 may be NULL (img_start, img_len when n_img = 0; text_pos when
+ * T_tot = 0).
  */
 typedef struct {
   int32_t B, n_img, N_tok, T_tot;
@@ -104,7 +106,7 @@ typedef struct {
  *   src + p*src_plane_stride + keep_idx[r]*src_stride
  * (token-major [N_tok, ...] tensors use planes = 1; position ids [P, N_tok]
  * use planes = P; head-major K/V [Hkv, N_tok, d] use planes = Hkv).
- * All strides and offsets in bytes.
+ * All strides and offsets in bytes.  dst may be NULL when no row is kept.
  */
 typedef struct {
   const void *src;

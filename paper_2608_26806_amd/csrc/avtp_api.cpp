@@ -22,11 +22,13 @@ int check_layout(const avtp_layout *lay, DevLayout *out) {
   if (!lay) return AVTP_ERR_INVALID_ARG;
   const int B = lay->B, n_img = lay->n_img, N = lay->N_tok, T = lay->T_tot;
   if (B < 1 || n_img < 0 || N < 1 || T < 0) return AVTP_ERR_INVALID_ARG;
-  if (!lay->cu_seqlens || !lay->img_start || !lay->img_len || !lay->cu_img || !lay->text_pos ||
-      !lay->cu_text || !lay->keep_total)
+  // the image arrays may be NULL without images, text_pos without text rows
+  // (an empty array may have no address)
+  if (!lay->cu_seqlens || !lay->cu_img || !lay->cu_text || !lay->keep_total ||
+      (n_img > 0 && (!lay->img_start || !lay->img_len)) || (T > 0 && !lay->text_pos))
     return AVTP_ERR_INVALID_ARG;
-  if (!lay->h_cu_seqlens || !lay->h_img_start || !lay->h_img_len || !lay->h_cu_img ||
-      !lay->h_text_pos || !lay->h_cu_text || !lay->h_keep_total)
+  if (!lay->h_cu_seqlens || !lay->h_cu_img || !lay->h_cu_text || !lay->h_keep_total ||
+      (n_img > 0 && (!lay->h_img_start || !lay->h_img_len)) || (T > 0 && !lay->h_text_pos))
     return AVTP_ERR_INVALID_ARG;
   if (n_img > AVTP_MAX_IMAGES) return AVTP_ERR_UNSUPPORTED;
   const int32_t *cs = lay->h_cu_seqlens, *ci = lay->h_cu_img, *ct = lay->h_cu_text;
@@ -319,7 +321,9 @@ static int check_tensors(const DevLayout &L, int64_t n_out, const avtp_tensor *t
   if (n_tensors > 0 && !tensors) return AVTP_ERR_INVALID_ARG;
   for (int i = 0; i < n_tensors; ++i) {
     const avtp_tensor &t = tensors[i];
-    if (!t.src || !t.dst || t.row_bytes < 1 || t.planes < 1) return AVTP_ERR_INVALID_ARG;
+    // (nothing is written when no row is kept: dst may then be NULL)
+    if (!t.src || (n_out > 0 && !t.dst) || t.row_bytes < 1 || t.planes < 1)
+      return AVTP_ERR_INVALID_ARG;
     if (t.src_stride < t.row_bytes || t.dst_stride < t.row_bytes) return AVTP_ERR_INVALID_ARG;
     if (t.planes > 1 && (t.src_plane_stride < (int64_t)L.N_tok * t.src_stride ||
                          t.dst_plane_stride < n_out * t.dst_stride))

@@ -300,3 +300,40 @@ def test_row_lse_without_text_rows_needs_no_query_pointer():
     # with text rows the same null pointers are rejected
     assert A.lib().avtp_row_lse(None, _dl().ref(), A.BF16, None, k, 4, 2, 128, 0.1, None, ws,
                                 buf.numel() - 256) == A.ERR_INVALID_ARG
+
+
+def test_empty_layout_arrays_may_be_null():
+    # arrays of length 0 need no address: the image arrays of a text-only
+    # batch, text_pos of a batch without text rows, a compaction's destination
+    # when no row is kept
+    lib = A.lib()
+
+    def layout(lay, null):
+        dl = _dl(lay)
+        for n in null:
+            setattr(dl.st, n, None)
+            setattr(dl.st, "h_" + n, None)
+        return dl
+
+    text_only = build_layout([[], []], 0, 3, 50)
+    assert text_only.n_img == 0
+    dl = layout(text_only, ("img_start", "img_len"))
+    assert A.score_workspace_bytes(dl, A.SCORE_ATTN, A.BF16, 4, 2, 128) > 0
+    images_only = build_layout([[7, 5]], 0, 0, 50)
+    assert images_only.T_tot == 0
+    dl = layout(images_only, ("text_pos",))
+    assert A.score_workspace_bytes(dl, A.SCORE_ATTN, A.BF16, 4, 2, 128) > 0
+    # the same nulls with arrays that are not empty are rejected
+    assert A.score_workspace_bytes(layout(build_layout([[7]], 1, 1, 50), ("text_pos",)),
+                                   A.SCORE_ATTN, A.BF16, 4, 2, 128) == 0
+    assert A.score_workspace_bytes(layout(build_layout([[7]], 1, 1, 50), ("img_len",)),
+                                   A.SCORE_ATTN, A.BF16, 4, 2, 128) == 0
+    # nothing kept: nothing is copied and no destination is needed
+    none_kept = build_layout([[6, 4]], 0, 0, 0)
+    dl = _dl(none_kept)
+    assert dl.N_out == 0
+    buf = torch.zeros(64, dtype=torch.uint8)
+    t = A._Tensor(buf.data_ptr(), None, 4, 4, 4, 1, 0, 0)
+    assert lib.avtp_compact(None, dl.ref(), None, 0, ctypes.byref(t), 1) == A.OK
+    t.src = None
+    assert lib.avtp_compact(None, dl.ref(), None, 0, ctypes.byref(t), 1) == A.ERR_INVALID_ARG
