@@ -1,7 +1,8 @@
 """Seeded random layouts through budget, selection and compaction, against
-the oracle: avtp_budget_select_compact (one call) and avtp_budget,
-avtp_select, avtp_compact (three calls) must both give the oracle's budgets,
-kept indices, cu_out and compacted tensors bit for bit.
+the oracle: avtp_budget_select_compact (one call), avtp_budget, avtp_select,
+avtp_compact (three calls) and avtp_budget then avtp_select_compact must all
+give the oracle's budgets, kept indices, cu_out and compacted tensors bit for
+bit.
 
 The layouts mix what the fixed workloads do not: a random number of text rows
 before every image (none included), empty and one-token images, images longer
@@ -142,5 +143,16 @@ def test_random_layout_one_call_and_three_calls(seed):
     assert np.array_equal(keep3.cpu().numpy()[:lay.N_out], keep_o)
     assert np.array_equal(cu3.cpu().numpy(), cu_o)
     for o, w in zip(out3, want):
+        assert np.array_equal(to_host_bits(o), to_host_bits(w))
+    assert not status.cpu().numpy().any()
+
+    # selection and compaction in one call, given the budgets
+    out2 = outs()
+    keep2, cu2 = A.select_compact(dl, s_d, bud3, [(x, o, d) for (x, d), o in zip(srcs, out2)],
+                                  status=status)
+    torch.cuda.synchronize()
+    assert np.array_equal(keep2.cpu().numpy()[:lay.N_out], keep_o)
+    assert np.array_equal(cu2.cpu().numpy(), cu_o)
+    for o, w in zip(out2, want):
         assert np.array_equal(to_host_bits(o), to_host_bits(w))
     assert not status.cpu().numpy().any()
