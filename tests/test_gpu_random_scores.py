@@ -123,3 +123,65 @@ def test_batch_without_text_rows():
                                           128 ** -0.5, "bf16")
     assert np.all(s_o[vis] == 0.0) and empty == {0, 2, 3}
     assert [int(x) for x in status.cpu().numpy()] == [A.FLAG_NO_TEXT_AFTER, 0, A.FLAG_NO_TEXT_AFTER]
+
+
+def _large_random_layout(rng):
+    """Up to 3 sequences of up to 11 images of up to 3,000 tokens, text between
+    the images and up to 700 text rows after them."""
+    cu_seqlens, img_start, img_len, cu_img, text_pos, cu_text = [0], [], [], [0], [], [0]
+    pos = 0
+    for _ in range(int(rng.integers(1, 4))):
+        for _ in range(int(rng.integers(1, 12))):
+            nt = int(rng.integers(0, 20))
+            text_pos.extend(range(pos, pos + nt))
+            pos += nt
+            n = int(rng.integers(1, 3000))
+            img_start.append(pos)
+            img_len.append(n)
+            pos += n
+        nt = int(rng.integers(1, 700))
+        text_pos.extend(range(pos, pos + nt))
+        pos += nt
+        cu_seqlens.append(pos)
+        cu_img.append(len(img_len))
+        cu_text.append(len(text_pos))
+    a = lambda v: np.asarray(v, dtype=np.int32)
+    return Layout(a(cu_seqlens), a(img_start), a(img_len), a(cu_img), a(text_pos), a(cu_text),
+                  np.zeros(len(cu_seqlens) - 1, np.int32))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_large_random_layout_scores(seed):
+    # tens of thousands of tokens, hundreds to thousands of text rows and up
+    # to 56 query heads: many key chunks, multi-stage query splits
+    from concurrent.futures import ThreadPoolExecutor
+    rng = np.random.default_rng(7000 + seed)
+    lay = _large_random_layout(rng)
+    Hkv = int(rng.choice([2, 4, 8]))
+    Hq = Hkv * int(rng.choice([1, 4, 7]))
+    d = 128
+    q = f32_to_bf16_bits(rng.standard_normal((lay.T_tot, Hq, d)).astype(np.float32))
+    k = f32_to_bf16_bits((rng.standard_normal((lay.N_tok, Hkv, d)) * 1.3).astype(np.float32))
+    say(f"[large random scores] seed {seed}: B={lay.B} images={lay.n_img} N_tok={lay.N_tok} "
+        f"T={lay.T_tot} Hq={Hq} Hkv={Hkv}")
+
+    def one(b):
+        return O.attn_scores(lay, q, k, Hq, Hkv, d ** -0.5, "bf16", seqs=[b])
+
+    with ThreadPoolExecutor(max_workers=min(8, lay.B)) as ex:
+        parts = list(ex.map(one, range(lay.B)))
+    s_o, isum_o = np.full(lay.N_tok, np.inf), np.zeros(lay.n_img)
+    lse_o = np.zeros((Hq, lay.T_tot))
+    for b, (sb, ib, lb, _) in enumerate(parts):
+        s0, s1 = int(lay.cu_seqlens[b]), int(lay.cu_seqlens[b + 1])
+        i0, i1 = int(lay.cu_img[b]), int(lay.cu_img[b + 1])
+        t0, t1 = int(lay.cu_text[b]), int(lay.cu_text[b + 1])
+        s_o[s0:s1], isum_o[i0:i1], lse_o[:, t0:t1] = sb[s0:s1], ib[i0:i1], lb[:, t0:t1]
+    dl = A.DeviceLayout(lay)
+    qd, kd = to_dev(q, "bf16"), to_dev(k, "bf16")
+    lse_g = A.row_lse(dl, qd, kd, d ** -0.5).cpu().numpy().astype(np.float64)
+    s_g, isum_g = A.score_attn(dl, qd, kd, d ** -0.5)
+    vis = lay.visual_mask()
+    assert_rel(lse_g, lse_o, 0.0, "row lse", abs_floor=TOL["bf16"])
+    assert_rel(s_g.cpu().numpy()[vis], s_o[vis], TOL["bf16"], "scores", abs_floor=1e-30)
+    assert_rel(isum_g.cpu().numpy(), isum_o, TOL["bf16"], "image sums", abs_floor=1e-30)
