@@ -10,6 +10,7 @@
 #include <stdint.h>
 
 #include "avtp_internal.h"
+#include "stream_load.h"
 #include "wave_ops.h"
 
 namespace avtp {
@@ -49,14 +50,9 @@ __device__ inline void acc8(const uint4 &x, const uint4 &y, float &dot, float &n
 }
 
 // Every row is read once, and the two tensors are far larger than the
-// caches: the loads are marked non-temporal so that they do not displace
-// cached data (measured 368 -> 334 us at 4 x 32,768 visual tokens of 4,096
-// bf16 values).
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-__device__ inline uint4 ld_stream(const uint4 *p) {
-  const u32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
-  return make_uint4(x.x, x.y, x.z, x.w);
-}
+// caches: the loads are non-temporal (ld_stream) so that they do not
+// displace cached data (measured 368 -> 334 us at 4 x 32,768 visual tokens of
+// 4,096 bf16 values).
 
 // three fp32 sums, as a value of wave::allreduce
 struct Sums3 {

@@ -412,7 +412,7 @@ __device__ inline void copy_listed(const CTensor &T, const int *lo, const int *l
   const int lane = threadIdx.x & ((1 << lpr_shift) - 1);
   const int per_pass = kThreads >> lpr_shift;
   for (int p = 0; p < T.planes; ++p)
-    copy_rows_batched<V>(T, p, (long long)(threadIdx.x >> lpr_shift), n, per_pass, lane,
+    copy_rows_batched<V, false>(T, p, (long long)(threadIdx.x >> lpr_shift), n, per_pass, lane,
                          [&](long long e, long long &j, long long &r) __attribute__((always_inline)) {
                            j = lj[e];
                            r = lo[e];
