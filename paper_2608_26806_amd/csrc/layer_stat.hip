@@ -22,6 +22,7 @@ __global__ void layer_attn_kernel(const float *__restrict__ img_sum, const int32
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
   double s = 0.0;
+#pragma unroll 8
   for (int i = cu_img[b]; i < cu_img[b + 1]; ++i) s += (double)img_sum[i];
   A[b] = (float)s;
 }
@@ -43,6 +44,8 @@ __global__ __launch_bounds__(kRankThreads) void layer_rank_kernel(const float *_
   for (int i = threadIdx.x; i < N; i += kRankThreads) {
     const float a = rank_key(A[(size_t)l * N + i]);
     int r = 1;
+    // eight layers' loads in flight at a time (the loop is latency-bound)
+#pragma unroll 8
     for (int m = 0; m < L; ++m) {
       const float v = rank_key(A[(size_t)m * N + i]);
       r += (v > a) || (v == a && m < l);
