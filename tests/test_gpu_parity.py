@@ -350,6 +350,32 @@ def test_compact_odd_row_sizes():
         assert torch.equal(out.cpu(), x.cpu()[torch.from_numpy(keep).long()])
 
 
+def test_compact_streaming_loads_every_vector_width():
+    # one launch that reads more than 256 MiB (so the source rows are read
+    # with non-temporal loads), with rows copied in 16-, 8-, 4-, 2- and
+    # 1-byte units: every output row bit-exact against the oracle
+    lay = build_layout([[20000, 20000]], 2, 3, 50)
+    dl = A.DeviceLayout(lay)
+    rng = np.random.default_rng(21)
+    keep = np.sort(rng.choice(lay.N_tok, dl.N_out, replace=False)).astype(np.int32)
+    keep_d = torch.from_numpy(keep).cuda()
+    g = torch.Generator(device="cuda").manual_seed(21)
+    srcs = [torch.randint(-2**31, 2**31 - 1, (lay.N_tok, 4096), dtype=torch.int32, device="cuda",
+                          generator=g)]                                       # 16 KB rows
+    for shape, dt in [((lay.N_tok, 3), torch.int64), ((lay.N_tok, 7), torch.float32),
+                      ((lay.N_tok, 33, 2), torch.bfloat16), ((lay.N_tok, 5), torch.int16),
+                      ((lay.N_tok, 3), torch.uint8)]:
+        srcs.append(torch.randint(0, 100, shape, dtype=torch.int32, device="cuda",
+                                  generator=g).to(dt))
+    read = dl.N_out * sum(x[0].numel() * x.element_size() for x in srcs)
+    assert read > 256 << 20
+    say(f"[compact] streaming loads: {read / 1e6:.0f} MB read, N_out={dl.N_out}")
+    outs = A.compact_new(dl, keep_d, [(x, 0) for x in srcs])
+    torch.cuda.synchronize()
+    for x, o in zip(srcs, outs):
+        assert np.array_equal(to_host_bits(o), O.compact(keep, to_host_bits(x)))
+
+
 def test_compact_out_of_range_index_leaves_row():
     # entries -1 and >= N_tok, some in the middle of a thread group's four
     # rows: those output rows keep what they held, all others are copied
