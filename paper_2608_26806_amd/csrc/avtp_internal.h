@@ -35,6 +35,7 @@ struct AttnPlan {
   int kchunk;     // keys per pass-1 chunk (multiple of 64)
   int nkc;        // chunks per sequence (max)
   int nkb;        // key blocks per (sequence, key head) in pass 2
+  int nkt2;       // 32-key tiles per wave in pass 2
   int nqs;        // query splits of pass 2 (column-sum planes per key head)
   int nsl;        // pass 2: each (sequence, key head)'s key blocks are dealt to nsl
                   // slices (kb mod nsl), so that there are units for all 8 XCDs
