@@ -32,6 +32,7 @@ struct AttnPlan {
   int G;          // query heads per key head
   int rows_max;   // max over sequences of G * T_b
   int nqb;        // query blocks per (sequence, key head) in pass 1
+  int nt1;        // 32-row query tiles per wave in pass 1
   int kchunk;     // keys per pass-1 chunk (multiple of 64)
   int nkc;        // chunks per sequence (max)
   int nkb;        // key blocks per (sequence, key head) in pass 2

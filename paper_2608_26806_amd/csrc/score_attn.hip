@@ -276,12 +276,12 @@ struct P1Args {
 // only in part takes a per-element masked variant.  Query rows are
 // token-major (the G heads of one text token adjacent), so a block's rows
 // span few positions and a block of early text rows stops at its last row.
-template <typename T, int D>
+template <typename T, int D, int NT>
 __global__ __launch_bounds__(kThreads, (Occ<T, D>::value)) void rowstats_kernel(P1Args a) {
   using G_ = Geo<T, D>;
   using MM = Mma<T>;
   using frag = typename MM::frag;
-  constexpr int NT = kTiles1, NS = G_::NS, ROWB = G_::ROWB, E = G_::E;
+  constexpr int NS = G_::NS, ROWB = G_::ROWB, E = G_::E;
   constexpr int QB = 4 * NT * 32;  // query rows per block
   constexpr int KS = kStage1;      // keys per LDS stage
   constexpr int TPS = KS / 32;     // key tiles per stage
@@ -1004,7 +1004,15 @@ hipError_t run_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P, co
   a.part_l = (float *)(ws + P.off_part_l);
   const int nunits = L.B * Hkv * P.nkc;
   const int grid = ((nunits + 7) / 8) * 8 * P.nqb;
-  hipLaunchKernelGGL((rowstats_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, a);
+  if constexpr (sizeof(T) == 2 && D == 128) {  // one query tile per wave on small grids (attn_plan)
+    if (P.nt1 == 1) {
+      hipLaunchKernelGGL((rowstats_kernel<T, D, 1>), dim3(grid), dim3(kThreads), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((rowstats_kernel<T, D, kTiles1>), dim3(grid), dim3(kThreads), 0, st, a);
+    }
+  } else {
+    hipLaunchKernelGGL((rowstats_kernel<T, D, kTiles1>), dim3(grid), dim3(kThreads), 0, st, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int rows = Hq * L.T_tot;
@@ -1067,35 +1075,55 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   AttnPlan P;
   P.G = Hq / Hkv;
   const int row_bytes = d * (dtype == AVTP_FP32 ? 4 : 2);
-  const int rows_per_block = 4 * kTiles1 * 32;                 // pass 1 query rows per block
   int nkt2 = tiles_pass2(row_bytes);                            // pass 2 key tiles per wave
   P.rows_max = P.G * L.max_text;
-  P.nqb = (P.rows_max + rows_per_block - 1) / rows_per_block;
-  if (P.nqb < 1) P.nqb = 1;
-  // split keys so that pass 1 launches about 2048 blocks (8 per CU); chunks
-  // of at least two stages, or one on a grid of less than one block per CU,
-  // where a block's latency is what counts
-  const long long base = (long long)L.B * Hkv * P.nqb;
-  long long want = (2048 + base - 1) / base;
-  if (want < 1) want = 1;
-  long long kc = (L.max_seqlen + want - 1) / want;
-  kc = ((kc + kStage - 1) / kStage) * kStage;
-  if (kc < 2 * kStage1) {
-    const long long two = (L.max_seqlen + 2 * kStage1 - 1) / (2 * kStage1);  // chunks of two stages
-    kc = base * two < 256 ? (kc < kStage1 ? kStage1 : kc) : 2 * kStage1;
+  // Pass 1 geometry for nt query tiles per wave: query blocks per unit and
+  // the key chunk.
+  auto pass1 = [&](int nt, int &nqb, long long &kc) {
+    const int rows_per_block = 4 * nt * 32;
+    nqb = (P.rows_max + rows_per_block - 1) / rows_per_block;
+    if (nqb < 1) nqb = 1;
+    // split keys so that pass 1 launches about 2048 blocks (8 per CU); chunks
+    // of at least two stages, or one on a grid of less than one block per CU,
+    // where a block's latency is what counts
+    const long long base = (long long)L.B * Hkv * nqb;
+    long long want = (2048 + base - 1) / base;
+    if (want < 1) want = 1;
+    kc = (L.max_seqlen + want - 1) / want;
+    kc = ((kc + kStage1 - 1) / kStage1) * kStage1;
+    if (kc < 2 * kStage1) {
+      const long long two = (L.max_seqlen + 2 * kStage1 - 1) / (2 * kStage1);  // chunks of two stages
+      kc = base * two < 256 ? (kc < kStage1 ? kStage1 : kc) : 2 * kStage1;
+    }
+    // Where that gives blocks of at most two stages but more than 512 of them
+    // (more than one round at two blocks per CU), a block's fixed latency
+    // (layout reads, query loads, the first stage's wait, the flush) outweighs
+    // its work: take chunks long enough for at most 512 blocks, one round.
+    // Two sequences of 8 images with 96 text rows: 1,024 blocks of two stages
+    // -> 512 of four, pass 1 33.3 -> 28.8 us (384 or 256 blocks: 34.7, 29.7).
+    if (kc <= 2 * kStage1 && base <= 512 && base * ((L.max_seqlen + kc - 1) / kc) > 512) {
+      const long long per = 512 / base;  // chunks per unit
+      long long k2 = (L.max_seqlen + per - 1) / per;
+      k2 = ((k2 + kStage1 - 1) / kStage1) * kStage1;
+      if (k2 > kc) kc = k2;
+    }
+    return base * ((L.max_seqlen + kc - 1) / kc);  // blocks
+  };
+  // Two query tiles per wave (a key fragment read from LDS serves two
+  // MFMAs).  A grid that fits in one round (at most 512 blocks) is bound by
+  // latency instead: there, for bf16 d = 128, blocks of one tile per wave
+  // (128 rows, more blocks and rows of closer positions) measured faster:
+  // one sequence of 4 x 729 tokens 13.4 -> 12.9 us, two sequences of 8
+  // images 28.4 -> 26.2 us; on the larger grids they were slower (8 x 16
+  // images 127-131 -> 134-137 us, 4 x 32 images 536-540 -> 602-606 us).
+  int nqb = 1;
+  long long kc = 0;
+  P.nt1 = kTiles1;
+  if (pass1(kTiles1, nqb, kc) <= 512 && dtype != AVTP_FP32 && d == 128) {
+    P.nt1 = 1;
+    pass1(1, nqb, kc);
   }
-  // Where that gives blocks of at most two stages but more than 512 of them
-  // (more than one round at two blocks per CU), a block's fixed latency
-  // (layout reads, query loads, the first stage's wait, the flush) outweighs
-  // its work: take chunks long enough for at most 512 blocks, one round.
-  // Two sequences of 8 images with 96 text rows: 1,024 blocks of two stages
-  // -> 512 of four, pass 1 33.3 -> 28.8 us (384 or 256 blocks: 34.7, 29.7).
-  if (kc <= 2 * kStage1 && base <= 512 && base * ((L.max_seqlen + kc - 1) / kc) > 512) {
-    const long long per = 512 / base;  // chunks per unit
-    long long k2 = (L.max_seqlen + per - 1) / per;
-    k2 = ((k2 + kStage1 - 1) / kStage1) * kStage1;
-    if (k2 > kc) kc = k2;
-  }
+  P.nqb = nqb;
   P.kchunk = (int)kc;
   P.nkc = (L.max_seqlen + P.kchunk - 1) / P.kchunk;
   if (P.nkc < 1) P.nkc = 1;
