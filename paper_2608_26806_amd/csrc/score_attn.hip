@@ -1004,15 +1004,10 @@ hipError_t run_row_lse(hipStream_t st, const DevLayout &L, const AttnPlan &P, co
   a.part_l = (float *)(ws + P.off_part_l);
   const int nunits = L.B * Hkv * P.nkc;
   const int grid = ((nunits + 7) / 8) * 8 * P.nqb;
-  if constexpr (sizeof(T) == 2 && D == 128) {  // one query tile per wave on small grids (attn_plan)
-    if (P.nt1 == 1) {
-      hipLaunchKernelGGL((rowstats_kernel<T, D, 1>), dim3(grid), dim3(kThreads), 0, st, a);
-    } else {
-      hipLaunchKernelGGL((rowstats_kernel<T, D, kTiles1>), dim3(grid), dim3(kThreads), 0, st, a);
-    }
-  } else {
+  if (P.nt1 == 1)  // one query tile per wave on small grids (attn_plan)
+    hipLaunchKernelGGL((rowstats_kernel<T, D, 1>), dim3(grid), dim3(kThreads), 0, st, a);
+  else
     hipLaunchKernelGGL((rowstats_kernel<T, D, kTiles1>), dim3(grid), dim3(kThreads), 0, st, a);
-  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int rows = Hq * L.T_tot;
@@ -1111,7 +1106,7 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   };
   // Two query tiles per wave (a key fragment read from LDS serves two
   // MFMAs).  A grid that fits in one round (at most 512 blocks) is bound by
-  // latency instead: there, for bf16 d = 128, blocks of one tile per wave
+  // latency instead: there blocks of one tile per wave
   // (128 rows, more blocks and rows of closer positions) measured faster:
   // one sequence of 4 x 729 tokens 13.4 -> 12.9 us, two sequences of 8
   // images 28.4 -> 26.2 us; on the larger grids they were slower (8 x 16
@@ -1119,7 +1114,7 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
   int nqb = 1;
   long long kc = 0;
   P.nt1 = kTiles1;
-  if (pass1(kTiles1, nqb, kc) <= 512 && dtype != AVTP_FP32 && d == 128) {
+  if (pass1(kTiles1, nqb, kc) <= 512) {
     P.nt1 = 1;
     pass1(1, nqb, kc);
   }
