@@ -63,8 +63,9 @@ struct Mma<float> {
 };
 
 // Register budget, two waves per SIMD (256 VGPRs per wave).  Pass 1 keeps
-// two 32-row query tiles per wave and four accumulator sets; pass 2 keeps up
-// to 96 registers of stationary key tiles, one accumulator set each.  fp32
+// at most two 32-row query tiles per wave and two accumulator sets per tile;
+// pass 2 keeps up to 96 registers of stationary key tiles, one accumulator
+// set each (fewer tiles on small grids, see attn_plan).  fp32
 // operands at d = 128 do not fit that budget and run one wave per SIMD.
 constexpr int kTiles1 = 2;
 template <typename T, int D>
@@ -266,8 +267,9 @@ struct P1Args {
 // row statistics of every query row: a reference m (log2 units) and the sum
 // l of 2^(z c log2e - m) over the row's visible keys of the chunk.
 //
-// Each wave holds two 32-row query tiles.  Per 32-key tile the MFMAs of both
-// tiles advance k-step by k-step, while the VALU turns the two accumulators
+// Each wave holds NT 32-row query tiles (two; one on grids that fit in one
+// round, see attn_plan).  Per 32-key tile the MFMAs of the NT tiles advance
+// k-step by k-step, while the VALU turns the two accumulators
 // of the previous key tile into exp2 sums (one FMA, one exp2 and one add per
 // logit), so no instruction waits on a result of the running MFMAs.  The
 // reference of a row is kept lazily: it is raised (and the row's sum
