@@ -1080,11 +1080,14 @@ AttnPlan attn_plan(const DevLayout &L, int Hq, int Hkv, int d, int dtype) {
     const int rows_per_block = 4 * nt * 32;
     nqb = (P.rows_max + rows_per_block - 1) / rows_per_block;
     if (nqb < 1) nqb = 1;
-    // split keys so that pass 1 launches about 2048 blocks (8 per CU); chunks
-    // of at least two stages, or one on a grid of less than one block per CU,
-    // where a block's latency is what counts
+    // split keys so that pass 1 launches about 1536 blocks (6 per CU, three
+    // rounds of two); chunks of at least two stages, or one on a grid of less
+    // than one block per CU, where a block's latency is what counts.  Against
+    // 2048 blocks: 8 sequences of 16 images 135 -> 129 us, 4 x 32 images of
+    // 1,024 tokens 488 -> 482 us sustained; 2560-4096 blocks were 3-4 %
+    // slower there
     const long long base = (long long)L.B * Hkv * nqb;
-    long long want = (2048 + base - 1) / base;
+    long long want = (1536 + base - 1) / base;
     if (want < 1) want = 1;
     kc = (L.max_seqlen + want - 1) / want;
     kc = ((kc + kStage1 - 1) / kStage1) * kStage1;
