@@ -41,7 +41,7 @@ def test_noalloc_matches_workspace_call_twice_then_smaller():
     need_gpu()
     A.lib()
     big = make_workload(5, payload=False)
-    say("[noalloc] config 5 (8.6 MiB of scratch)")
+    say("[noalloc] config 5 (7.6 MiB of scratch)")
     _run_both(big)
     say("[noalloc] config 5 again")
     _run_both(big)
